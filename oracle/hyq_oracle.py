@@ -1,0 +1,335 @@
+"""CPU oracle for HyQuant hybrid-precision prefill attention.
+
+TEST INFRASTRUCTURE ONLY.  This module is the plain, slow reference that the
+HIP path is checked against.  Only the test suite, ``__graft_entry__.smoke()``
+and the ``cpu_baseline`` leg of ``bench.py`` may import it; the product
+library never calls it and shares no code with it.
+
+It follows the paper step by step:
+
+* Algorithm 1 (App. A.1, Vertical Token Identification): window exclusion,
+  tail-query proxy, GQA-native scoring, budget k and top-k.
+* Algorithm 2 (App. A.2, HyQuant Prefill), Stage 1: the partition of the
+  key positions into quantized / vertical-line / window sets (also the
+  disjoint-partition equation of Section 4.1); Stage 2: per-tile symmetric
+  quantization with scale max|x|/c_B.
+* Eq. (prefill_hybrid) of Section 4.2: softmax over the concatenation of the
+  dequantized-key logits and the full-precision logits, times the
+  concatenation of the dequantized and full-precision values, here with a
+  causal mask by original key position.  Attention is computed row-wise in
+  float64 (not online), then rounded to float32.
+
+Readings where the paper is silent or ambiguous (all fixed here, the HIP
+path follows the same ones):
+
+* the window is the last W keys [L-W, L); P = L - W is the prefix length;
+* the vertical set is chosen per KV head, from the tail proxy summed over the
+  g query heads of the group (the 1/t, 1/g means are dropped: they do not
+  change the ranking);
+* budget: k = 0 if the ratio is 0 or P = 0, else min(P, max(1, ceil(P*r)))
+  with r given in parts per million and integer ceiling division;
+* top-k ties go to the lowest position, -0 equals +0; the vertical index
+  list is returned in ascending order;
+* quantization blocks of ``block`` rows run over the compacted K_Q sequence
+  (vertical-line rows removed) and over the original query rows; the scale
+  is fl32(amax / c) and the code rint_half_even(fl32(x / s)) clamped to
+  [-c, c]; an all-zero block has scale 0 and codes 0; c = 127 for 8-bit and
+  7 for 4-bit; Q is always 8-bit when K/V are quantized;
+* causality holds by original key position in every segment;
+* bits = 16 disables quantization: every key takes the full-precision path.
+
+Floating-point orders that the paper leaves open are pinned so that the
+selection is reproducible bit for bit:
+
+* tail proxy: for each query head r of the group, float32 sum of its tail
+  rows in ascending row order starting from +0; then the g partial sums are
+  added in head order;
+* score: float32 products qsum[d]*K[p,d] (separate multiply, no fused
+  multiply-add), then the upper half of the vector is folded onto the lower
+  half repeatedly (128 -> 64 -> ... -> 1).
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+C_INT8 = 127
+C_INT4 = 7
+
+
+# ---------------------------------------------------------------------------
+# helpers
+# ---------------------------------------------------------------------------
+
+def bf16_to_f32(bits: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns (uint16/int16) -> float32, exact."""
+    b = np.ascontiguousarray(bits).view(np.uint16)
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def code_bound(bits: int) -> int:
+    """c_B of Algorithm 2, Stage 2 (127 for INT8); 7 for the 4-bit reading."""
+    if bits == 8:
+        return C_INT8
+    if bits == 4:
+        return C_INT4
+    raise ValueError("no code bound for bits=%d" % bits)
+
+
+def sizes(L: int, W: int, budget_ppm: int, block: int = 64) -> dict:
+    """Prefix length P, vertical budget k and block counts.
+
+    P = max(0, L - W) (Algorithm 1, window exclusion); k = min(P, max(1,
+    ceil(P * r))) (Algorithm 1, budget), r = budget_ppm / 1e6, and k = 0 when
+    the budget is 0 or P = 0.  nQ = P - k keys are quantized.
+    """
+    if L < 1 or W < 0 or not (0 <= budget_ppm <= 1_000_000) or block < 1:
+        raise ValueError("bad sizes arguments")
+    P = max(0, L - W)
+    if budget_ppm == 0 or P == 0:
+        k = 0
+    else:
+        k = min(P, max(1, -(-(P * budget_ppm) // 1_000_000)))
+    nQ = P - k
+    return dict(P=P, k=k, nQ=nQ,
+                n_qblk=-(-L // block),
+                n_kvblk=-(-nQ // block))
+
+
+# ---------------------------------------------------------------------------
+# Algorithm 1: vertical token identification
+# ---------------------------------------------------------------------------
+
+def tail_proxy(Qf: np.ndarray, Hkv: int, W: int) -> np.ndarray:
+    """Summed tail query per KV head: qsum[b, j, :] (float32).
+
+    Algorithm 1, tail-query proxy with t = min(W, L_Q); GQA reshape of the
+    query heads into (H_KV, g) with consecutive grouping.  Summed, not
+    averaged (scale does not change the ranking).  Pinned order: per query
+    head, ascending rows from +0; then heads in order.
+    """
+    B, Hq, L, D = Qf.shape
+    g = Hq // Hkv
+    t = min(W, L)
+    Qg = Qf.reshape(B, Hkv, g, L, D)
+    total = None
+    for r in range(g):
+        a = np.zeros((B, Hkv, D), dtype=np.float32)
+        for i in range(L - t, L):
+            a = a + Qg[:, :, r, i, :]
+        total = a if total is None else total + a
+    return total
+
+
+def fold_sum(prod: np.ndarray) -> np.ndarray:
+    """Sum over the last axis by repeatedly adding the upper half onto the
+    lower half (the pinned reduction tree); the axis length must be a power
+    of two."""
+    v = prod
+    n = v.shape[-1]
+    if n & (n - 1):
+        raise ValueError("head dim must be a power of two")
+    while n > 1:
+        h = n // 2
+        v = v[..., :h] + v[..., h:n]
+        n = h
+    return v[..., 0]
+
+
+def scores(qsum: np.ndarray, Kf: np.ndarray, P: int) -> np.ndarray:
+    """S[b, j, p] = qsum[b, j] . K[b, j, p] for p in [0, P) (Algorithm 1,
+    GQA-native einsum over the non-window prefix), float32, pinned tree."""
+    prod = qsum[:, :, None, :] * Kf[:, :, :P, :]
+    return fold_sum(prod)
+
+
+def topk_ascending(S: np.ndarray, k: int) -> np.ndarray:
+    """The k largest scores of the last axis (ties: lowest position first),
+    returned as ascending positions (eq. vl_topk; Algorithm 1, TopK)."""
+    S = S + np.float32(0.0)          # -0 -> +0
+    out = np.empty(S.shape[:-1] + (k,), dtype=np.int32)
+    for ix in np.ndindex(*S.shape[:-1]):
+        order = np.argsort(-S[ix], kind="stable")   # stable: equal scores keep position order
+        out[ix] = np.sort(order[:k]).astype(np.int32)
+    return out
+
+
+def select_vertical(Qb: np.ndarray, Kb: np.ndarray, Hkv: int, W: int, budget_ppm: int):
+    """Algorithm 1 on bf16 inputs.  Returns (idx [B,Hkv,k] int32 ascending,
+    S [B,Hkv,P] float32 or None when k = 0)."""
+    B, Hq, L, D = Qb.shape
+    sz = sizes(L, W, budget_ppm)
+    P, k = sz["P"], sz["k"]
+    if k == 0:
+        return np.zeros((B, Hkv, 0), dtype=np.int32), None
+    if min(W, L) < 1:
+        raise ValueError("a vertical budget needs a window of at least one query")
+    qsum = tail_proxy(bf16_to_f32(Qb), Hkv, W)
+    S = scores(qsum, bf16_to_f32(Kb), P)
+    return topk_ascending(S, k), S
+
+
+# ---------------------------------------------------------------------------
+# Algorithm 2, Stages 1-2: partition and per-block quantization
+# ---------------------------------------------------------------------------
+
+def compaction(idx: np.ndarray, P: int) -> np.ndarray:
+    """kq_pos[b, j, :] = [0, P) minus the vertical positions, ascending
+    (Algorithm 2 Stage 1 partition; the K_Q index set of Algorithm 4)."""
+    B, Hkv, k = idx.shape
+    out = np.empty((B, Hkv, P - k), dtype=np.int32)
+    for b in range(B):
+        for j in range(Hkv):
+            out[b, j] = np.setdiff1d(np.arange(P, dtype=np.int32), idx[b, j])
+    return out
+
+
+def quantize_rows(x: np.ndarray, block: int, c: int):
+    """Per-block symmetric quantization of rows x [n, D] (float32).
+
+    Algorithm 2 Stage 2: for each block of ``block`` consecutive rows, s =
+    max|x| / c_B in float32, code = round(x / s) (half to even, float32
+    division), clamped to [-c, c]; s = 0 gives codes 0.  Returns (codes int8
+    [n, D], scales float32 [ceil(n/block)]).
+    """
+    n, D = x.shape
+    nb = -(-n // block)
+    codes = np.zeros((n, D), dtype=np.int8)
+    scales = np.zeros(nb, dtype=np.float32)
+    for i in range(nb):
+        blk = x[i * block:(i + 1) * block]
+        amax = np.float32(np.max(np.abs(blk)))
+        s = np.float32(amax / np.float32(c))
+        scales[i] = s
+        if s != 0:
+            codes[i * block:(i + 1) * block] = np.clip(np.rint(blk / s), -c, c).astype(np.int8)
+    return codes, scales
+
+
+def quantize(Qb, Kb, Vb, idx, W: int, bits: int, block: int = 64):
+    """Algorithm 2, Stages 1-2 on bf16 inputs.
+
+    Returns a dict: kq_pos [B,Hkv,nQ]; q_codes int8 [B,Hq,L,D], q_scale
+    [B,Hq,n_qblk]; k_codes / v_codes int8 [B,Hkv,nQ,D] (values in [-c, c],
+    not packed), k_scale / v_scale [B,Hkv,n_kvblk].  bits = 16 returns only
+    kq_pos (nothing is quantized).
+    """
+    B, Hq, L, D = Qb.shape
+    Hkv = Kb.shape[1]
+    P = max(0, L - W)
+    kq_pos = compaction(idx, P)
+    out = dict(kq_pos=kq_pos)
+    if bits == 16:
+        return out
+    c = code_bound(bits)
+    nQ = kq_pos.shape[2]
+    n_qblk = -(-L // block)
+    n_kvblk = -(-nQ // block)
+    q_codes = np.zeros((B, Hq, L, D), np.int8)
+    q_scale = np.zeros((B, Hq, n_qblk), np.float32)
+    for b in range(B):
+        for h in range(Hq):
+            q_codes[b, h], q_scale[b, h] = quantize_rows(bf16_to_f32(Qb[b, h]), block, C_INT8)
+    k_codes = np.zeros((B, Hkv, nQ, D), np.int8)
+    v_codes = np.zeros((B, Hkv, nQ, D), np.int8)
+    k_scale = np.zeros((B, Hkv, n_kvblk), np.float32)
+    v_scale = np.zeros((B, Hkv, n_kvblk), np.float32)
+    for b in range(B):
+        for j in range(Hkv):
+            rows = kq_pos[b, j]
+            k_codes[b, j], k_scale[b, j] = quantize_rows(bf16_to_f32(Kb[b, j][rows]), block, c)
+            v_codes[b, j], v_scale[b, j] = quantize_rows(bf16_to_f32(Vb[b, j][rows]), block, c)
+    out.update(q_codes=q_codes, q_scale=q_scale, k_codes=k_codes, k_scale=k_scale,
+               v_codes=v_codes, v_scale=v_scale)
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Eq. (prefill_hybrid): hybrid-precision causal attention
+# ---------------------------------------------------------------------------
+
+def _head_operands(Qb, Kb, Vb, b, h, Hkv, W, bits, block, idx, qz):
+    """Logit ingredients of one (batch, query head): for every key, its
+    original position, and the pieces of its logit and value."""
+    B, Hq, L, D = Qb.shape
+    g = Hq // Hkv
+    j = h // g
+    P = max(0, L - W)
+    if bits == 16:
+        fp_pos = np.arange(L)
+    else:
+        fp_pos = np.concatenate([idx[b, j].astype(np.int64), np.arange(P, L)])
+    ops = dict(
+        fp_pos=fp_pos,
+        Q=bf16_to_f32(Qb[b, h]).astype(np.float64),
+        Kfp=bf16_to_f32(Kb[b, j][fp_pos]).astype(np.float64),
+        Vfp=bf16_to_f32(Vb[b, j][fp_pos]).astype(np.float64),
+    )
+    if bits != 16:
+        nQ = qz["kq_pos"].shape[2]
+        blk = np.arange(nQ) // block
+        ops.update(
+            q_pos=qz["kq_pos"][b, j].astype(np.int64),
+            qcode=qz["q_codes"][b, h].astype(np.float64),
+            qscale=qz["q_scale"][b, h].astype(np.float64),
+            kcode=qz["k_codes"][b, j].astype(np.float64),
+            kscale=qz["k_scale"][b, j][blk].astype(np.float64),
+            vhat=qz["v_scale"][b, j][blk].astype(np.float64)[:, None] * qz["v_codes"][b, j].astype(np.float64),
+        )
+    return ops
+
+
+def _rows_logits(ops, rows, D, bits, block):
+    """Concatenated logits [len(rows), nkeys], values and key positions."""
+    alpha = 1.0 / math.sqrt(D)
+    Zfp = alpha * (ops["Q"][rows] @ ops["Kfp"].T)
+    if bits == 16:
+        return Zfp, ops["Vfp"], ops["fp_pos"]
+    # Quantized keys: alpha * s_Q * s_K * <q_code, k_code> (Algorithm 2, Segment A).
+    Zq = alpha * (ops["qcode"][rows] @ ops["kcode"].T) \
+        * ops["qscale"][rows // block][:, None] * ops["kscale"][None, :]
+    Z = np.concatenate([Zq, Zfp], axis=1)
+    Vall = np.concatenate([ops["vhat"], ops["Vfp"]], axis=0)
+    pos = np.concatenate([ops["q_pos"], ops["fp_pos"]])
+    return Z, Vall, pos
+
+
+def attention(Qb, Kb, Vb, W: int, bits: int, idx, qz=None, block: int = 64,
+              heads=None, rows=None, return_weights: bool = False, chunk: int = 1024):
+    """Causal hybrid attention output in float32.
+
+    ``heads``: list of (b, h) to evaluate (default: all); ``rows``: query rows
+    (default: all), shared by every listed head.  Returns O [len(heads),
+    len(rows), D] float32 (and, if ``return_weights``, the float64 weight
+    matrices over original key positions [len(heads), len(rows), L]).
+    """
+    B, Hq, L, D = Qb.shape
+    Hkv = Kb.shape[1]
+    if heads is None:
+        heads = [(b, h) for b in range(B) for h in range(Hq)]
+    rows = np.arange(L) if rows is None else np.asarray(rows, dtype=np.int64)
+    O = np.zeros((len(heads), len(rows), D), dtype=np.float32)
+    Wfull = np.zeros((len(heads), len(rows), L)) if return_weights else None
+    for hi, (b, h) in enumerate(heads):
+        ops = _head_operands(Qb, Kb, Vb, b, h, Hkv, W, bits, block, idx, qz)
+        for c0 in range(0, len(rows), chunk):
+            r = rows[c0:c0 + chunk]
+            Z, Vall, pos = _rows_logits(ops, r, D, bits, block)
+            Z = np.where(pos[None, :] <= r[:, None], Z, -np.inf)     # causal, original positions
+            m = Z.max(axis=1, keepdims=True)
+            E = np.exp(Z - m)
+            den = E.sum(axis=1, keepdims=True)
+            O[hi, c0:c0 + len(r)] = ((E @ Vall) / den).astype(np.float32)
+            if return_weights:
+                Wfull[hi, c0:c0 + len(r)][:, pos] = E / den
+    return (O, Wfull) if return_weights else O
+
+
+def prefill(Qb, Kb, Vb, Hkv: int, W: int, budget_ppm: int, bits: int, block: int = 64,
+            heads=None, rows=None):
+    """The whole path of Algorithm 2: selection, quantization, attention."""
+    idx, _ = select_vertical(Qb, Kb, Hkv, W, budget_ppm)
+    qz = quantize(Qb, Kb, Vb, idx, W, bits, block)
+    O = attention(Qb, Kb, Vb, W, bits, idx, qz, block, heads=heads, rows=rows)
+    return dict(idx=idx, O=O, **qz)

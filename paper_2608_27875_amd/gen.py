@@ -1,0 +1,96 @@
+"""Seeded synthetic inputs for the HyQuant prefill path.
+
+This module only draws inputs; it holds none of the method's arithmetic
+(no selection, quantization or attention).  Both the HIP path and the CPU
+oracle consume exactly the bf16 bit patterns produced here.
+
+Workload recipe (stands in for real-model activations, which are not
+available): Q, K, V ~ N(0, 1) drawn as float32 and rounded to bf16; a set
+of "vertical-line" key rows per KV head (position 0 plus a fraction of
+random positions) gets 4 * (unit direction of the summed tail queries of
+that KV head's query group) added; finally four fixed K channels are scaled
+by 10 on every key (outlier channels, the case per-block quantization
+handles worst).  Shapes follow the paper's models (GQA 32q/8kv and 40q/8kv,
+head_dim 128, Section 5.1 and the configuration table of App. B).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+OUTLIER_CHANNELS = (3, 47, 85, 122)
+
+# The five workloads: shapes, window, vertical budget (parts per million of
+# the non-window prefix), K/V bit-width and the planted vertical-line fraction.
+CONFIGS = {
+    1: dict(B=1, Hq=1, Hkv=1, L=1024, D=128, W=64, budget_ppm=20000, bits=8, plant=0.01),
+    2: dict(B=1, Hq=32, Hkv=8, L=8192, D=128, W=128, budget_ppm=20000, bits=8, plant=0.01),
+    3: dict(B=1, Hq=32, Hkv=8, L=32768, D=128, W=256, budget_ppm=10000, bits=8, plant=0.01),
+    4: dict(B=1, Hq=32, Hkv=8, L=131072, D=128, W=512, budget_ppm=5000, bits=8, plant=0.01),
+    5: dict(B=4, Hq=40, Hkv=8, L=16384, D=128, W=256, budget_ppm=20000, bits=8, plant=0.05),
+}
+# Config 5 is a sweep over these two axes.
+SWEEP5_BUDGETS = (5000, 20000, 50000)
+SWEEP5_BITS = (8, 4)
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 to bf16 (round-to-nearest-even); returns uint16 bit patterns."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32)
+    bias = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
+    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    """Exact widening of bf16 bit patterns to float32."""
+    return (np.ascontiguousarray(b).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def generate(seed: int, stream: int, B: int, Hq: int, Hkv: int, L: int, D: int,
+             W: int, plant: float, outliers=OUTLIER_CHANNELS, **_unused):
+    """Draw one seeded input set.
+
+    Returns a dict with uint16 (bf16 bit pattern) arrays ``Q`` [B,Hq,L,D],
+    ``K`` and ``V`` [B,Hkv,L,D], and ``planted``: a list over (b, j) of the
+    sorted planted key positions.  ``stream`` separates workloads that share a
+    seed (configs use their number).
+    """
+    if Hq % Hkv:
+        raise ValueError("Hq must be a multiple of Hkv")
+    g = Hq // Hkv
+    rng = np.random.default_rng([int(seed), int(stream)])
+    Q = f32_to_bf16_bits(rng.standard_normal((B, Hq, L, D), dtype=np.float32))
+    K = f32_to_bf16_bits(rng.standard_normal((B, Hkv, L, D), dtype=np.float32))
+    V = f32_to_bf16_bits(rng.standard_normal((B, Hkv, L, D), dtype=np.float32))
+
+    t = min(max(W, 1), L)                 # tail length used for the planted direction
+    n_plant = min(L - 1, int(np.floor(plant * L + 0.5)))
+    planted = []
+    for b in range(B):
+        for j in range(Hkv):
+            tail = bf16_bits_to_f32(Q[b, j * g:(j + 1) * g, L - t:L, :]).astype(np.float64)
+            u = tail.sum(axis=(0, 1))
+            nrm = np.sqrt(np.dot(u, u))
+            u = u / nrm if nrm > 0 else np.zeros(D)
+            pos = np.concatenate([[0], rng.choice(np.arange(1, L), n_plant, replace=False)]) \
+                if L > 1 else np.array([0])
+            pos = np.sort(pos.astype(np.int64))
+            rows = bf16_bits_to_f32(K[b, j, pos, :]).astype(np.float64) + 4.0 * u[None, :]
+            K[b, j, pos, :] = f32_to_bf16_bits(rows.astype(np.float32))
+            planted.append(pos)
+    for c in outliers:
+        if c < D:
+            col = bf16_bits_to_f32(K[..., c]) * np.float32(10.0)
+            K[..., c] = f32_to_bf16_bits(col)
+    return dict(Q=Q, K=K, V=V, planted=planted)
+
+
+def generate_config(cfg_id: int, seed: int = 0, **overrides):
+    """Inputs for one of the five named workloads (``overrides`` may change the
+    budget or bit-width of the sweep config; the drawn tensors do not depend on
+    them)."""
+    cfg = dict(CONFIGS[cfg_id])
+    cfg.update(overrides)
+    data = generate(seed, cfg_id, **cfg)
+    data["cfg"] = cfg
+    return data

@@ -1,0 +1,140 @@
+"""Brute-force re-derivations used to pin the oracle on tiny inputs.
+
+These share no code with the oracle: selection is by counting ranks,
+quantization is exact rational arithmetic rounded to float32 by hand, and
+attention is a scalar loop over keys with math.exp.  Only tiny inputs.
+"""
+from __future__ import annotations
+
+import math
+from fractions import Fraction
+
+import numpy as np
+
+
+def bf16_value(bits) -> float:
+    """bf16 bit pattern -> Python float (exact), by decoding the fields."""
+    b = int(bits) & 0xFFFF
+    sign = -1.0 if b >> 15 else 1.0
+    e = (b >> 7) & 0xFF
+    m = b & 0x7F
+    if e == 0:
+        return sign * m * 2.0 ** (-133)            # subnormal: m * 2^-7 * 2^-126
+    if e == 0xFF:
+        raise ValueError("inf/nan not expected")
+    return sign * (1.0 + m / 128.0) * 2.0 ** (e - 127)
+
+
+def round_to_f32(x: Fraction) -> Fraction:
+    """Correctly round an exact rational to the nearest float32 (ties to even)."""
+    if x == 0:
+        return Fraction(0)
+    sign = -1 if x < 0 else 1
+    a = abs(x)
+    e = math.floor(math.log2(a.numerator) - math.log2(a.denominator))
+    # fix possible off-by-one from the float log
+    while Fraction(2) ** e > a:
+        e -= 1
+    while Fraction(2) ** (e + 1) <= a:
+        e += 1
+    e = max(e, -126)                                # subnormal range shares the 2^-149 grid
+    ulp = Fraction(2) ** (e - 23)
+    q, r = divmod(a, ulp)
+    q = int(q)
+    if r > ulp / 2 or (r == ulp / 2 and q % 2 == 1):
+        q += 1
+    val = q * ulp
+    if val >= Fraction(2) ** 128:
+        raise OverflowError
+    return sign * val
+
+
+def round_half_even(x: Fraction) -> int:
+    fl = math.floor(x)
+    r = x - fl
+    if r > Fraction(1, 2) or (r == Fraction(1, 2) and fl % 2 == 1):
+        return fl + 1
+    return fl
+
+
+def quant_block_exact(vals, c: int):
+    """Symmetric block quantization with exact rationals: s = fl32(amax/c),
+    code = clamp(rint(fl32(x/s)), -c, c).  ``vals`` are float32-exact numbers."""
+    fr = [Fraction(float(v)) for v in vals]
+    amax = max(abs(v) for v in fr)
+    s = round_to_f32(amax / c)
+    if s == 0:
+        return [0] * len(fr), 0.0
+    codes = [max(-c, min(c, round_half_even(round_to_f32(v / s)))) for v in fr]
+    return codes, float(s)
+
+
+def topk_by_rank(S, k: int):
+    """Position p is chosen iff fewer than k positions beat it, where p' beats p
+    when S[p'] > S[p], or S[p'] == S[p] and p' < p.  Ascending output."""
+    S = [float(v) for v in S]          # -0.0 == 0.0 in Python comparisons
+    chosen = []
+    for p in range(len(S)):
+        beat = sum(1 for q in range(len(S)) if S[q] > S[p] or (S[q] == S[p] and q < p))
+        if beat < k:
+            chosen.append(p)
+    return chosen
+
+
+def attention_rows(Qv, Kv, Vv, L, W, bits, block, idx_list, qcodes, qscales,
+                   kcodes, kscales, vcodes, vscales):
+    """Scalar-loop hybrid attention for one (batch, head).
+
+    Qv, Kv, Vv: lists of float rows (original positions).  idx_list: the
+    vertical positions of this KV head.  q/k/v codes and scales are per
+    quantized row (already expanded: kscales[n] is the scale of row n's block).
+    Returns a list of output rows (floats) and the weight rows.
+    """
+    D = len(Qv[0])
+    alpha = 1.0 / math.sqrt(D)
+    P = max(0, L - W)
+    vl = set(idx_list)
+    qpos = [p for p in range(P) if p not in vl]          # quantized keys, ascending
+    where = {p: n for n, p in enumerate(qpos)}
+    out, weights = [], []
+    for t in range(L):
+        zs, vals, poss = [], [], []
+        for p in range(t + 1):
+            if bits != 16 and p in where:
+                n = where[p]
+                dot = sum(int(qcodes[t][d]) * int(kcodes[n][d]) for d in range(D))
+                z = alpha * qscales[t // block] * kscales[n] * dot
+                val = [vscales[n] * int(vcodes[n][d]) for d in range(D)]
+            else:
+                z = alpha * math.fsum(Qv[t][d] * Kv[p][d] for d in range(D))
+                val = list(Vv[p])
+            zs.append(z)
+            vals.append(val)
+            poss.append(p)
+        m = max(zs)
+        ws = [math.exp(z - m) for z in zs]
+        den = math.fsum(ws)
+        row = [math.fsum(w * v[d] for w, v in zip(ws, vals)) / den for d in range(D)]
+        wrow = [0.0] * L
+        for p, w in zip(poss, ws):
+            wrow[p] = w / den
+        out.append(row)
+        weights.append(wrow)
+    return out, weights
+
+
+def int_select(Qint, Kint, Hkv, W, k):
+    """Selection on integer-valued inputs in exact int64 arithmetic:
+    qsum = sum over group and tail, S = qsum . K, rank by (-S, p)."""
+    B, Hq, L, D = Qint.shape
+    g = Hq // Hkv
+    t = min(W, L)
+    P = max(0, L - W)
+    out = np.zeros((B, Hkv, k), dtype=np.int64)
+    for b in range(B):
+        for j in range(Hkv):
+            qs = Qint[b, j * g:(j + 1) * g, L - t:, :].astype(np.int64).sum(axis=(0, 1))
+            S = Kint[b, j, :P, :].astype(np.int64) @ qs
+            order = np.lexsort((np.arange(P), -S))
+            out[b, j] = np.sort(order[:k])
+    return out
