@@ -1,0 +1,249 @@
+#!/usr/bin/env python
+"""Benchmark of the HyQuant hybrid-precision prefill path on one MI355X.
+
+A step is one pass of the whole hot path over one synthetic layer:
+hyq_select_vertical -> hyq_quantize -> hyq_attn_prefill, with Q/K/V already
+resident in HBM.  Default workload: GQA 32 query / 8 KV heads, head dim 128,
+32768 tokens, window 256, vertical budget 1%, 8-bit K/V, float32 output (the
+launch configuration the parity tests check at full size).
+
+Prints one JSON line.  ``value`` is the algorithmic causal attention FLOPs
+(4 * D * Hq * B * L(L+1)/2) per second of the whole step, in TFLOP/s;
+``roofline`` describes the attention kernel alone (timed with HIP events on
+the stream it runs on); ``cpu_baseline`` is the CPU oracle on a bounded
+sample of the same layer.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+INT8_PEAK_TOPS = 5000.0        # MI355X dense int8 MFMA, TOP/s
+F16_PEAK_TFLOPS = 2500.0       # MI355X dense f16/bf16 MFMA, TFLOP/s
+BLENDED_PEAK = 1.0 / (0.5 / INT8_PEAK_TOPS + 0.5 / F16_PEAK_TFLOPS)   # int8 QK^T + f16 PV
+HBM_PEAK_GBS = 8000.0
+
+
+def causal_flops(B, Hq, L, D):
+    return 4.0 * D * Hq * B * L * (L + 1) / 2.0
+
+
+def attn_src_digest():
+    h = hashlib.sha256()
+    with open(os.path.join(ROOT, "paper_2608_27875_amd", "csrc", "attn_prefill.hip"), "rb") as f:
+        h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload):
+    """HBM bytes per attention launch from rocprofv3 FETCH_SIZE / WRITE_SIZE
+    counters (profiles/attn_traffic.json), only if taken on this kernel source."""
+    p = os.path.join(ROOT, "profiles", "attn_traffic.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        rec = json.load(open(p))
+    except ValueError:
+        return None
+    if rec.get("kernel_src_sha") != attn_src_digest() or rec.get("workload") != workload:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(d, cfg, flops_total, budget_s):
+    """The oracle (untuned) on a bounded sample: full selection and
+    quantization of the layer, attention for a few heads x rows; the
+    whole-layer time is extrapolated from the attention FLOPs of the sample."""
+    import numpy as np
+    from oracle import hyq_oracle as orc
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    L, W, D, Hq = cfg["L"], cfg["W"], 128, cfg["Hq"]
+    t0 = time.perf_counter()
+    idx, _ = orc.select_vertical(d["Q"], d["K"], cfg["Hkv"], W, cfg["budget_ppm"])
+    t_sel = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    qz = orc.quantize(d["Q"], d["K"], d["V"], idx, W, cfg["bits"])
+    t_quant = time.perf_counter() - t0
+    heads = [(0, h) for h in range(0, Hq, max(1, Hq // 4))][:4]
+    rng = np.random.default_rng(0)
+    n_rows = 64
+    t_attn, f_attn = 0.0, 0.0
+    while True:
+        rows = np.sort(rng.choice(L, size=n_rows, replace=False))
+        t0 = time.perf_counter()
+        orc.attention(d["Q"], d["K"], d["V"], W, cfg["bits"], idx, qz, heads=heads, rows=rows)
+        dt = time.perf_counter() - t0
+        t_attn += dt
+        f_attn += len(heads) * float(np.sum(4.0 * D * (rows + 1)))
+        if t_attn + t_sel + t_quant > budget_s or n_rows >= 4096:
+            break
+        n_rows *= 2
+    est = t_sel + t_quant + t_attn * (flops_total / f_attn)
+    return {
+        "value": flops_total / est / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+        "sample": (f"full selection ({t_sel:.2f} s) and quantization ({t_quant:.2f} s) of the layer; "
+                   f"attention for {len(heads)} heads x {n_rows}-row random row sets "
+                   f"({t_attn:.2f} s for {f_attn:.3e} FLOP); whole-layer time extrapolated "
+                   f"to {est:.1f} s"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=3, help="workload id (1-5); 3 = 32k GQA")
+    ap.add_argument("--bits", type=int, default=None, help="override K/V bit-width (16, 8, 4)")
+    ap.add_argument("--budget-ppm", type=int, default=None)
+    ap.add_argument("--out-bf16", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=20.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--seed", type=int, default=0)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: the operator is single-GPU (heads shard with no "
+              "communication, see the design notes); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2608_27875_amd as hyq
+    from paper_2608_27875_amd import gen
+
+    cfg = dict(gen.CONFIGS[args.config])
+    if args.bits is not None:
+        cfg["bits"] = args.bits
+    if args.budget_ppm is not None:
+        cfg["budget_ppm"] = args.budget_ppm
+    print(f"[bench] generating config {args.config}: {cfg}", file=sys.stderr, flush=True)
+    d = gen.generate_config(args.config, seed=args.seed)
+    dev = torch.device("cuda:0")
+
+    def t(x):
+        return torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev)
+
+    Q, K, V = t(d["Q"]), t(d["K"]), t(d["V"])
+    shape = hyq.Shape(B=cfg["B"], Hq=cfg["Hq"], Hkv=cfg["Hkv"], L=cfg["L"], window=cfg["W"],
+                      budget_ppm=cfg["budget_ppm"], bits_kv=cfg["bits"])
+    out_dtype = 1 if args.out_bf16 else 0
+    bufs = hyq.alloc_buffers(shape, dev, out_dtype)
+    z = bufs["sizes"]
+    scale = 1.0 / math.sqrt(shape.D)
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev:
+            ev[0].record(stream)
+        hyq.hyq_select_vertical(shape, Q, K, bufs["idx"], None, bufs["ws"], stream)
+        if ev:
+            ev[1].record(stream)
+        hyq.hyq_quantize(shape, Q, K, V, bufs["idx"], bufs["q_codes"], bufs["q_scale"],
+                         bufs["k_codes"], bufs["k_scale"], bufs["v_codes"], bufs["v_scale"],
+                         bufs["kq_pos"], stream)
+        if ev:
+            ev[2].record(stream)
+        hyq.hyq_attn_prefill(shape, Q, K, V, bufs["idx"], bufs["q_codes"], bufs["q_scale"],
+                             bufs["k_codes"], bufs["k_scale"], bufs["v_codes"], bufs["v_scale"],
+                             bufs["kq_pos"], scale, bufs["out"], out_dtype, stream)
+        if ev:
+            ev[3].record(stream)
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+    sel = [e[0].elapsed_time(e[1]) for e in evs]
+    qnt = [e[1].elapsed_time(e[2]) for e in evs]
+    att = [e[2].elapsed_time(e[3]) for e in evs]
+    attn_ms = float(np.mean(att))
+
+    flops = causal_flops(shape.B, shape.Hq, shape.L, shape.D)
+    value = flops / (ms_step * 1e-3) / 1e12
+    attn_tflops = flops / (attn_ms * 1e-3) / 1e12
+    # algorithmic bytes of the select and quantize kernels (one read of each
+    # input row they need, one write of each output)
+    sel_bytes = (shape.B * shape.Hq * min(shape.window, shape.L) * 256 +
+                 shape.B * shape.Hkv * z["P"] * 256 + z["idx_bytes"]) if z["k"] else 0
+    q_bytes = 0
+    if shape.bits_kv != 16:
+        q_bytes = (shape.B * shape.Hq * shape.L * 256 + 2 * shape.B * shape.Hkv * z["nQ"] * 256 +
+                   z["q_codes_bytes"] + z["k_codes_bytes"] + z["v_codes_bytes"] +
+                   z["q_scale_bytes"] + 2 * z["kv_scale_bytes"] + z["kq_pos_bytes"] + z["idx_bytes"])
+    workload = (f"gqa{shape.Hq}q{shape.Hkv}kv_d{shape.D}_B{shape.B}_L{shape.L}_W{shape.window}"
+                f"_r{shape.budget_ppm}ppm_kv{shape.bits_kv}bit")
+    traffic = load_traffic(workload)
+    planted = d["planted"]
+    idx = bufs["idx"].cpu().numpy()
+    recall = []
+    for bj in range(shape.B * shape.Hkv):
+        pp = [p for p in planted[bj].tolist() if p < z["P"]]
+        if pp and z["k"]:
+            recall.append(len(set(pp) & set(idx.reshape(-1, z["k"])[bj].tolist())) /
+                          min(len(pp), z["k"]))
+    rec = {
+        "metric": "hybrid prefill attention TFLOP/s + % MFMA peak (GQA 32q/8kv, d128, 32k)",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "i8+f16" if shape.bits_kv != 16 else "bf16",
+        "data": "synthetic (seeded Gaussian Q/K/V, planted vertical lines, x10 outlier K channels)",
+        "config": {"workload": workload, "B": shape.B, "Hq": shape.Hq, "Hkv": shape.Hkv,
+                   "L": shape.L, "D": shape.D, "window": shape.window,
+                   "budget_ppm": shape.budget_ppm, "bits_kv": shape.bits_kv,
+                   "out": "bf16" if out_dtype else "f32", "k": z["k"], "parallelism": "none"},
+        "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": INT8_PEAK_TOPS,
+                     "unit": "TFLOP/s", "frac": round(attn_tflops / INT8_PEAK_TOPS, 4),
+                     "traffic": traffic, "kernel": "attn_prefill_kernel"},
+        "ms_per_layer": {"total": round(ms_step, 4), "attention": round(attn_ms, 4),
+                         "select": round(float(np.mean(sel)), 4),
+                         "quantize": round(float(np.mean(qnt)), 4)},
+        "attention_tflops": round(attn_tflops, 2),
+        "frac_int8_peak": round(attn_tflops / INT8_PEAK_TOPS, 4),
+        "frac_blended_ceiling": round(attn_tflops / BLENDED_PEAK, 4),
+        "select_gbs": round(sel_bytes / (np.mean(sel) * 1e-3) / 1e9, 1) if sel_bytes else None,
+        "quantize_gbs": round(q_bytes / (np.mean(qnt) * 1e-3) / 1e9, 1) if q_bytes else None,
+        "planted_recall": round(float(np.mean(recall)), 4) if recall else None,
+    }
+    if not args.no_cpu_baseline:
+        print(f"[bench] cpu baseline (oracle, ~{args.cpu_budget_s:.0f} s)", file=sys.stderr,
+              flush=True)
+        rec["cpu_baseline"] = cpu_baseline(d, cfg, flops, args.cpu_budget_s)
+    else:
+        rec["cpu_baseline"] = None
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -165,7 +165,8 @@ def select_vertical(Qb: np.ndarray, Kb: np.ndarray, Hkv: int, W: int, budget_ppm
         return np.zeros((B, Hkv, 0), dtype=np.int32), None
     if min(W, L) < 1:
         raise ValueError("a vertical budget needs a window of at least one query")
-    qsum = tail_proxy(bf16_to_f32(Qb), Hkv, W)
+    t = min(W, L)
+    qsum = tail_proxy(bf16_to_f32(Qb[:, :, L - t:, :]), Hkv, W)   # only the tail rows are read
     S = scores(qsum, bf16_to_f32(Kb), P)
     return topk_ascending(S, k), S
 
@@ -195,16 +196,15 @@ def quantize_rows(x: np.ndarray, block: int, c: int):
     """
     n, D = x.shape
     nb = -(-n // block)
-    codes = np.zeros((n, D), dtype=np.int8)
-    scales = np.zeros(nb, dtype=np.float32)
-    for i in range(nb):
-        blk = x[i * block:(i + 1) * block]
-        amax = np.float32(np.max(np.abs(blk)))
-        s = np.float32(amax / np.float32(c))
-        scales[i] = s
-        if s != 0:
-            codes[i * block:(i + 1) * block] = np.clip(np.rint(blk / s), -c, c).astype(np.int8)
-    return codes, scales
+    padded = np.zeros((nb * block, D), dtype=np.float32)   # zero rows do not change max|x|
+    padded[:n] = x
+    blocks = padded.reshape(nb, block, D)
+    amax = np.abs(blocks).max(axis=(1, 2))
+    scales = (amax / np.float32(c)).astype(np.float32)      # float32 division per block
+    safe = np.where(scales == 0, np.float32(1.0), scales)
+    codes = np.clip(np.rint(blocks / safe[:, None, None]), -c, c)
+    codes[scales == 0] = 0
+    return codes.reshape(nb * block, D)[:n].astype(np.int8), scales
 
 
 def quantize(Qb, Kb, Vb, idx, W: int, bits: int, block: int = 64):

@@ -1,0 +1,195 @@
+// C ABI of libhyq: argument validation, derived sizes, error reporting, and
+// the launches of the selection, quantization and attention kernels.
+// Nothing here allocates device memory or reads device memory back.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "hyq_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int ok() {
+  g_err[0] = '\0';
+  return HYQ_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Shape checks shared by every entry point, then the derived sizes
+// (Algorithm 1: P = max(0, L - W); k = min(P, max(1, ceil(P r))), 0 if r = 0
+// or P = 0).
+int check_shape(const hyq_shape* s, hyq_sizes* z) {
+  if (!s) return fail(HYQ_EINVAL, "shape is NULL");
+  if (s->B < 1 || s->Hq < 1 || s->Hkv < 1 || s->L < 1 || s->D < 1)
+    return fail(HYQ_EINVAL, "B, Hq, Hkv, L, D must be >= 1 (got %d, %d, %d, %d, %d)", s->B,
+                s->Hq, s->Hkv, s->L, s->D);
+  if (s->Hq % s->Hkv) return fail(HYQ_EINVAL, "Hq (%d) must be a multiple of Hkv (%d)", s->Hq, s->Hkv);
+  if (s->window < 0) return fail(HYQ_EINVAL, "window must be >= 0 (got %d)", s->window);
+  if (s->budget_ppm < 0 || s->budget_ppm > 1000000)
+    return fail(HYQ_EINVAL, "budget_ppm must be in [0, 1000000] (got %d)", s->budget_ppm);
+  if (s->block < 1) return fail(HYQ_EINVAL, "block must be >= 1 (got %d)", s->block);
+  if (s->bits_kv != 16 && s->bits_kv != 8 && s->bits_kv != 4)
+    return fail(HYQ_EUNSUPPORTED, "bits_kv must be 16, 8 or 4 (got %d)", s->bits_kv);
+  if (s->D != hyq::kHeadDim)
+    return fail(HYQ_EUNSUPPORTED, "head dim %d not supported (only %d)", s->D, hyq::kHeadDim);
+  if (s->block != hyq::kBlock)
+    return fail(HYQ_EUNSUPPORTED, "block %d not supported (only %d)", s->block, hyq::kBlock);
+  if (s->Hq / s->Hkv > 8)
+    return fail(HYQ_EUNSUPPORTED, "GQA group size %d not supported (at most 8)", s->Hq / s->Hkv);
+  // 32-bit element offsets inside one head; whole tensors use 64-bit offsets
+  if ((int64_t)s->L * s->D > (int64_t)1 << 30)
+    return fail(HYQ_EUNSUPPORTED, "sequence length %d too long", s->L);
+
+  const int64_t L = s->L, W = s->window;
+  const int64_t P = L > W ? L - W : 0;
+  int64_t k = 0;
+  if (s->budget_ppm > 0 && P > 0) {
+    k = (P * s->budget_ppm + 999999) / 1000000;
+    if (k < 1) k = 1;
+    if (k > P) k = P;
+  }
+  if (k > 0 && (W < L ? W : L) < 1)
+    return fail(HYQ_EINVAL, "a vertical budget needs window >= 1 (the tail-query proxy averages "
+                            "the last min(W, L) queries)");
+  const int64_t nQ = P - k;
+  const int64_t bs = s->block;
+  memset(z, 0, sizeof *z);
+  z->P = (int32_t)P;
+  z->k = (int32_t)k;
+  z->nQ = (int32_t)nQ;
+  z->n_qblk = (int32_t)((L + bs - 1) / bs);
+  z->n_kvblk = (int32_t)((nQ + bs - 1) / bs);
+  const size_t B = s->B, Hq = s->Hq, Hkv = s->Hkv, D = s->D;
+  const size_t slots = (size_t)z->n_kvblk * bs;
+  const bool quant = s->bits_kv != 16;
+  z->kv_row_bytes = !quant ? 0 : (s->bits_kv == 8 ? (int32_t)D : (int32_t)D / 2);
+  z->idx_bytes = B * Hkv * (size_t)k * 4;
+  z->scores_bytes = B * Hkv * (size_t)P * 4;
+  if (quant) {
+    z->kq_pos_bytes = B * Hkv * slots * 4;
+    z->q_codes_bytes = B * Hq * (size_t)L * D;
+    z->q_scale_bytes = B * Hq * (size_t)z->n_qblk * 4;
+    z->k_codes_bytes = B * Hkv * slots * z->kv_row_bytes;
+    z->v_codes_bytes = B * Hkv * (size_t)z->n_kvblk * D * (size_t)(bs * s->bits_kv / 8);
+    z->kv_scale_bytes = B * Hkv * (size_t)z->n_kvblk * 4;
+  }
+  z->select_ws_bytes = k > 0 ? align256(B * Hkv * D * 4) + align256(z->scores_bytes) : 0;
+  return HYQ_OK;
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(HYQ_EHIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+HYQ_API const char* hyq_strerror(int code) {
+  switch (code) {
+    case HYQ_OK: return "success";
+    case HYQ_EINVAL: return "invalid argument";
+    case HYQ_EUNSUPPORTED: return "unsupported configuration";
+    case HYQ_EHIP: return "HIP runtime error";
+    default: return "unknown error";
+  }
+}
+
+HYQ_API const char* hyq_last_error(void) { return g_err; }
+
+HYQ_API int hyq_sizes_for(const hyq_shape* shape, hyq_sizes* out) {
+  if (!out) return fail(HYQ_EINVAL, "sizes output is NULL");
+  hyq_sizes z;
+  const int rc = check_shape(shape, &z);
+  if (rc) return rc;
+  *out = z;
+  return ok();
+}
+
+HYQ_API int hyq_select_vertical(const hyq_shape* shape, const void* Q, const void* K, int32_t* idx,
+                        float* scores, void* ws, size_t ws_bytes, void* stream) {
+  hyq_sizes z;
+  const int rc = check_shape(shape, &z);
+  if (rc) return rc;
+  if (z.k == 0) return ok();
+  if (!Q || !K || !idx) return fail(HYQ_EINVAL, "Q, K and idx must be non-NULL");
+  if (!ws || ws_bytes < z.select_ws_bytes)
+    return fail(HYQ_EINVAL, "workspace too small: %zu bytes given, %zu needed", ws_bytes,
+                z.select_ws_bytes);
+  float* qsum = static_cast<float*>(ws);
+  float* sc = scores ? scores
+                     : reinterpret_cast<float*>(static_cast<char*>(ws) +
+                                                align256((size_t)shape->B * shape->Hkv *
+                                                         shape->D * 4));
+  return hip_status(hyq::launch_select(*shape, z, static_cast<const uint16_t*>(Q),
+                                       static_cast<const uint16_t*>(K), idx, sc, qsum,
+                                       static_cast<hipStream_t>(stream)),
+                    "hyq_select_vertical launch");
+}
+
+HYQ_API int hyq_quantize(const hyq_shape* shape, const void* Q, const void* K, const void* V,
+                 const int32_t* idx, int8_t* q_codes, float* q_scale, void* k_codes,
+                 float* k_scale, void* v_codes, float* v_scale, int32_t* kq_pos, void* stream) {
+  hyq_sizes z;
+  const int rc = check_shape(shape, &z);
+  if (rc) return rc;
+  if (shape->bits_kv == 16) return ok();
+  if (!Q || !K || !V || !q_codes || !q_scale)
+    return fail(HYQ_EINVAL, "Q, K, V, q_codes and q_scale must be non-NULL");
+  if (z.k > 0 && !idx) return fail(HYQ_EINVAL, "idx must be non-NULL when k > 0");
+  if (z.n_kvblk > 0 && (!k_codes || !k_scale || !v_codes || !v_scale || !kq_pos))
+    return fail(HYQ_EINVAL,
+                "k_codes, k_scale, v_codes, v_scale and kq_pos must be non-NULL when nQ > 0");
+  return hip_status(
+      hyq::launch_quantize(*shape, z, static_cast<const uint16_t*>(Q),
+                           static_cast<const uint16_t*>(K), static_cast<const uint16_t*>(V), idx,
+                           q_codes, q_scale, static_cast<uint8_t*>(k_codes), k_scale,
+                           static_cast<uint8_t*>(v_codes), v_scale, kq_pos,
+                           static_cast<hipStream_t>(stream)),
+      "hyq_quantize launch");
+}
+
+HYQ_API int hyq_attn_prefill(const hyq_shape* shape, const void* Q, const void* K, const void* V,
+                     const int32_t* idx, const int8_t* q_codes, const float* q_scale,
+                     const void* k_codes, const float* k_scale, const void* v_codes,
+                     const float* v_scale, const int32_t* kq_pos, float softmax_scale,
+                     void* out, int32_t out_dtype, void* stream) {
+  hyq_sizes z;
+  const int rc = check_shape(shape, &z);
+  if (rc) return rc;
+  if (!Q || !K || !V || !out) return fail(HYQ_EINVAL, "Q, K, V and out must be non-NULL");
+  if (out_dtype != 0 && out_dtype != 1)
+    return fail(HYQ_EINVAL, "out_dtype must be 0 (float32) or 1 (bf16), got %d", out_dtype);
+  if (!(softmax_scale > 0.0f) || softmax_scale == INFINITY)
+    return fail(HYQ_EINVAL, "softmax_scale must be positive and finite");
+  if (shape->bits_kv != 16) {
+    if (z.k > 0 && !idx) return fail(HYQ_EINVAL, "idx must be non-NULL when k > 0");
+    if (!q_codes || !q_scale) return fail(HYQ_EINVAL, "q_codes and q_scale must be non-NULL");
+    if (z.n_kvblk > 0 && (!k_codes || !k_scale || !v_codes || !v_scale || !kq_pos))
+      return fail(HYQ_EINVAL,
+                  "k_codes, k_scale, v_codes, v_scale and kq_pos must be non-NULL when nQ > 0");
+  }
+  return hip_status(
+      hyq::launch_attn_prefill(
+          *shape, z, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K),
+          static_cast<const uint16_t*>(V), idx, q_codes, q_scale,
+          static_cast<const uint8_t*>(k_codes), k_scale, static_cast<const uint8_t*>(v_codes),
+          v_scale, kq_pos, softmax_scale, out, out_dtype, static_cast<hipStream_t>(stream)),
+      "hyq_attn_prefill launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,132 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
+same seeded inputs.  Selection indices, scores, partition, codes and scales
+bit-exact; attention output within max-abs 2e-3 and mean-abs 2e-4 of the
+oracle's float32 result."""
+import zlib
+
+import numpy as np
+import pytest
+
+import gpu_common as gc
+from oracle import hyq_oracle as orc
+from paper_2608_27875_amd import gen
+
+pytestmark = pytest.mark.gpu
+
+# (name, B, Hq, Hkv, L, W, budget_ppm, bits): small enough for the full oracle,
+# several 64-key tiles and 32-row query tiles, ragged tails.
+SMALL = [
+    ("cfg1", 1, 1, 1, 1024, 64, 20000, 8),
+    ("gqa4_ragged", 1, 8, 2, 1000, 64, 20000, 8),
+    ("int4_b2", 2, 8, 2, 777, 100, 50000, 4),
+    ("g5", 1, 10, 2, 600, 48, 30000, 8),
+    ("g8_int4", 1, 16, 2, 400, 64, 20000, 4),
+    ("mha3", 2, 3, 3, 333, 20, 60000, 8),
+    ("bits16", 1, 4, 1, 500, 32, 20000, 16),
+    ("window_only", 1, 4, 1, 700, 96, 0, 8),
+    ("uniform_no_window", 1, 4, 1, 650, 0, 0, 8),
+    ("window_covers_all", 1, 4, 1, 200, 256, 20000, 8),
+    ("all_prefix_vertical", 1, 4, 1, 300, 40, 1000000, 8),
+    ("tiny", 1, 2, 1, 17, 4, 100000, 8),
+    ("one_token", 1, 2, 1, 1, 1, 0, 8),
+    ("one_block_exact", 1, 4, 1, 128, 64, 0, 4),
+]
+
+
+def _inputs(name, B, Hq, Hkv, L, W, plant=0.02, seed=0):
+    return gen.generate(seed, zlib.crc32(name.encode()) % 10007, B=B, Hq=Hq, Hkv=Hkv, L=L, D=128,
+                        W=max(W, 1), plant=plant)
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_small_full_parity(case):
+    name, B, Hq, Hkv, L, W, ppm, bits = case
+    print(f"case {name}", flush=True)
+    d = _inputs(name, B, Hq, Hkv, L, W)
+    shape = gc.hyq.Shape(B=B, Hq=Hq, Hkv=Hkv, L=L, window=W, budget_ppm=ppm, bits_kv=bits)
+    g = gc.run_gpu(shape, d)
+    idx, qz = gc.check_select_quant(shape, d, g)
+    O = orc.attention(d["Q"], d["K"], d["V"], W, bits, idx, qz)
+    mx, mean = gc.attention_error(g["out"].reshape(O.shape), O)
+    print(f"  max-abs {mx:.3e} mean-abs {mean:.3e}", flush=True)
+    assert mx <= gc.TOL_MAX and mean <= gc.TOL_MEAN
+
+
+def test_deterministic_and_bf16_output():
+    d = _inputs("det", 1, 8, 2, 900, 64)
+    shape = gc.hyq.Shape(B=1, Hq=8, Hkv=2, L=900, window=64, budget_ppm=20000, bits_kv=8)
+    g1 = gc.run_gpu(shape, d)
+    g2 = gc.run_gpu(shape, d)
+    for k in ("idx", "q_codes", "k_codes", "v_codes", "kq_pos", "out"):
+        np.testing.assert_array_equal(g1[k], g2[k], err_msg=k)
+    # bf16 output is the round-to-nearest-even of the float32 output
+    import torch
+    gb = gc.run_gpu(shape, d, out_dtype=1)
+    ref = torch.from_numpy(g1["out"]).to(torch.bfloat16).float().numpy()
+    np.testing.assert_array_equal(gb["out"], ref)
+
+
+def _big(cfg_id, n_heads, n_rows, seed=0, **over):
+    cfg = dict(gen.CONFIGS[cfg_id])
+    cfg.update(over)
+    print(f"config {cfg_id} {over}: generating", flush=True)
+    d = gen.generate_config(cfg_id, seed=seed)
+    return cfg, d
+
+
+def _check_big(cfg, d, n_heads, n_rows, seed):
+    shape = gc.shape_of(cfg)
+    print("  running HIP path", flush=True)
+    g = gc.run_gpu(shape, d, keep_out_on_gpu=True)
+    print("  oracle selection + quantization", flush=True)
+    idx, qz = gc.check_select_quant(shape, d, g)
+    rng = np.random.default_rng(seed)
+    all_heads = [(b, h) for b in range(shape.B) for h in range(shape.Hq)]
+    pick = rng.choice(len(all_heads), size=min(n_heads, len(all_heads)), replace=False)
+    heads = [all_heads[i] for i in sorted(pick)]
+    rows = gc.sample_rows(shape.L, shape.window, n_rows, seed)
+    print(f"  oracle attention on {len(heads)} heads x {len(rows)} rows", flush=True)
+    O = orc.attention(d["Q"], d["K"], d["V"], shape.window, shape.bits_kv, idx, qz,
+                      heads=heads, rows=rows)
+    out = g["out_dev"]
+    import torch
+    rt = torch.from_numpy(rows).to(out.device)
+    Og = np.stack([out[b, h].index_select(0, rt).cpu().numpy() for b, h in heads])
+    mx, mean = gc.attention_error(Og, O)
+    print(f"  max-abs {mx:.3e} mean-abs {mean:.3e}", flush=True)
+    assert mx <= gc.TOL_MAX and mean <= gc.TOL_MEAN
+
+
+@pytest.mark.timeout(300)
+def test_config2_8k_gqa():
+    cfg, d = _big(2, 32, 256)
+    _check_big(cfg, d, 32, 256, seed=2)
+
+
+@pytest.mark.timeout(300)
+def test_config3_32k_headline():
+    """The workload and launch configuration the benchmark times (float32 out)."""
+    cfg, d = _big(3, 4, 512)
+    _check_big(cfg, d, 4, 512, seed=3)
+
+
+@pytest.mark.timeout(600)
+def test_config4_128k():
+    cfg, d = _big(4, 2, 256)
+    _check_big(cfg, d, 2, 256, seed=4)
+
+
+@pytest.fixture(scope="module")
+def cfg5_data():
+    print("config 5: generating", flush=True)
+    return gen.generate_config(5, seed=0)
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("ppm", gen.SWEEP5_BUDGETS)
+@pytest.mark.parametrize("bits", gen.SWEEP5_BITS)
+def test_config5_sweep(cfg5_data, ppm, bits):
+    cfg = dict(gen.CONFIGS[5])
+    cfg.update(budget_ppm=ppm, bits=bits)
+    print(f"config 5 budget {ppm} bits {bits}", flush=True)
+    _check_big(cfg, cfg5_data, 2, 256, seed=5 + ppm + bits)
