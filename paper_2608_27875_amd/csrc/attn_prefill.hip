@@ -22,6 +22,14 @@
 // V^T tile in LDS stores each 16-key group in the matching order
 // [0-3, 8-11, 4-7, 12-15].
 //
+// Quantized tiles run through a three-buffer LDS ring fed from registers:
+// while tile c is computed, tile c+1 (loaded into registers during tile
+// c-1) is converted and written to LDS and tile c+2 is loaded, so global
+// latency is covered by a whole tile and each barrier waits only for LDS
+// writes.  The P V product of tile c-1 is issued interleaved with the
+// softmax of tile c (one MFMA per weight pair) so that the matrix cores and
+// the vector ALUs overlap within each wave.
+//
 // V scales are folded into the exponent: P' = 2^(y - m + log2(sV/sVref))
 // with sVref a power of two >= every sV of the head, so P' <= 1 fits f16 and
 // the accumulator holds O * l / sVref.  The row sum l adds P' * (sVref/sV)
@@ -34,25 +42,18 @@ namespace hyq {
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 typedef _Float16 v2h __attribute__((ext_vector_type(2)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
-#ifndef HYQ_ATTN_NB
-#define HYQ_ATTN_NB 1
-#endif
-constexpr int kNB = HYQ_ATTN_NB;          // 32-query MFMA column blocks per wave
 constexpr int kTile = 64;
 constexpr int kWaves = 4;                 // waves per workgroup (one per SIMD)
 constexpr int kThreads = kWaves * 64;
-constexpr int kStageThreads = kThreads;
-constexpr int kNBuf = 3;                  // quantized tiles c-1, c, c+1 resident
-constexpr float kLazy = 8.0f;             // rescale only when the max grows by > 2^8
-// instruction classes of __builtin_amdgcn_sched_group_barrier
-constexpr int kSchedMfma = 0x008;
-constexpr int kSchedDsRead = 0x100;
+constexpr float kLazy = 8.0f;             // general path: rescale only when the max grows by > 2^8
+constexpr float kFastMax = 32768.0f;      // fast path: largest accepted weight sum of a lane
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kMinusBig = -1.0e30f;
 
@@ -60,17 +61,29 @@ constexpr float kMinusBig = -1.0e30f;
 // rows on distinct banks.
 // int8 K tile: 64 rows of 128 B with no padding; the 16-byte chunk j of row r
 // is stored at slot j ^ (r % 8), which keeps 16-byte reads of 8 consecutive
-// rows on distinct banks and lets a wave fill 8 rows with one 1 KB direct
-// global-to-LDS load.
+// rows on distinct banks.
 constexpr int kKRowI8 = kHeadDim;
 constexpr int kKPitchBf = kHeadDim * 2 + 16;    // bf16 K row
 constexpr int kVPitch = kTile * 2 + 16;          // one channel of 64 f16/bf16 keys
 constexpr int kVBytes = kHeadDim * kVPitch;
 
-struct QBuf {                       // one quantized tile
+// Tile metadata: kq_pos of the 64 slots, the bits of sK and sV (read from
+// LDS rather than with scalar loads, whose counter would also wait for every
+// pending LDS read), and one slot that absorbs the stores of the other
+// staging threads so that staging needs no branch.
+constexpr int kMetaSK = kTile, kMetaSV = kTile + 1, kMetaSink = kTile + 2;
+struct KBuf {                       // K codes and metadata of one quantized tile
   alignas(16) uint8_t k[kTile * kKRowI8];
+  int32_t pos[kTile + 4];
+};
+struct VBuf {                       // V of one quantized tile as f16 V^T
   alignas(16) uint8_t v[kVBytes];
-  int32_t pos[kTile];
+};
+// Quantized segment: tile c reads K(c) from kb[c%2] and V(c-1) from
+// vb[(c-1)%2] while K(c+1) is written to kb[(c+1)%2] and V(c) to vb[c%2].
+struct QRing {
+  KBuf kb[2];
+  VBuf vb[2];
 };
 struct FBuf {                       // one full-precision tile
   alignas(16) uint8_t k[kTile * kKPitchBf];
@@ -78,7 +91,7 @@ struct FBuf {                       // one full-precision tile
   int32_t pos[kTile];
 };
 union Smem {
-  QBuf q[kNBuf];
+  QRing q;
   FBuf f;
 };
 
@@ -139,88 +152,98 @@ __device__ __forceinline__ int vslot(int e) {
 }
 
 // ---------------------------------------------------------------------------
-// Quantized tiles: each thread prefetches its share of tile c+1 from global
-// memory into registers while tile c is computed, then converts and writes it
-// into the other LDS buffer (one barrier per tile).
+// Quantized tiles, staged through registers: K codes (compacted order), V
+// codes (channel-major), kq_pos and the two block scales of one tile.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int kswz(int row, int chunk) {
   return row * kKRowI8 + ((chunk ^ (row & 7)) << 4);
 }
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void glob_void_t;
-
-// Group 0, 8-bit K: direct global -> LDS loads, two 1 KB instructions per
-// wave (LDS slots P = row*8 + slot, lane i of an instruction fills slot
-// base + i and reads the global chunk that belongs there).  Asynchronous:
-// the issuing waves wait (vmcnt) before the barrier that publishes the tile.
-__device__ __forceinline__ void k_direct_issue(uint8_t* kdst, const uint8_t* __restrict__ kc,
-                                               int wave_in_group, int lane) {
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int base = (wave_in_group * 2 + i) * 64;
-    const int P = base + lane;
-    const int row = P >> 3, slot = P & 7;
-    const int chunk = slot ^ (row & 7);
-    __builtin_amdgcn_global_load_lds((glob_void_t*)(kc + row * kKRowI8 + chunk * 16),
-                                     (lds_void_t*)(kdst + base * 16), 16, 0, 0);
-  }
-}
-
-// Group 0, 4-bit K: one 16-byte packed chunk per thread (32 channels of one
-// row), expanded to int8 (16*code) and stored as two swizzled chunks.
-__device__ __forceinline__ uint4 k4_load(const uint8_t* __restrict__ kc, int tid) {
-  return reinterpret_cast<const uint4*>(kc)[tid];
-}
-__device__ __forceinline__ void k4_store(uint8_t* kdst, uint4 w, int tid) {
-  const int row = tid >> 2, j4 = tid & 3;
-  uint32_t o[8];
-  i4x8_to_i8(w.x, o[0], o[1]);
-  i4x8_to_i8(w.y, o[2], o[3]);
-  i4x8_to_i8(w.z, o[4], o[5]);
-  i4x8_to_i8(w.w, o[6], o[7]);
-  *reinterpret_cast<uint4*>(kdst + kswz(row, 2 * j4)) = make_uint4(o[0], o[1], o[2], o[3]);
-  *reinterpret_cast<uint4*>(kdst + kswz(row, 2 * j4 + 1)) = make_uint4(o[4], o[5], o[6], o[7]);
-}
-
-// Group 1: V codes (channel-major in global) and kq_pos of a tile, loaded
-// into registers during the MFMA step and converted/stored during the VALU
-// step.  V -> f16 [128][kVPitch] in the permuted key order.
+// (native vectors: aggregate copies of HIP's uint4 would go through memory)
 template <int BITS>
-struct VTileRegs {
-  uint4 v[BITS == 8 ? 2 : 1];
-  int32_t pos;
+struct StageRegs {
+  v4u k[BITS == 8 ? 2 : 1];     // 16-byte chunks tid, tid+256 of a K tile
+  v4u v[BITS == 8 ? 2 : 1];     // same for a V tile
+  int32_t meta;                 // threads 0..63: kq_pos; 64, 65: sK, sV bits (K's tile)
 };
 
+// Everything one wave needs for the quantized segment.
+struct SegA {
+  const uint8_t* kc0;
+  const uint8_t* vc0;
+  const int32_t* kq0;
+  const float* ks0;
+  const float* vs0;
+  int n;              // quantized tiles to scan
+  int t0;             // first query row of the wave
+  float cq;           // alpha * log2(e) * s_Q
+  float inv_vref;
+  int lane, half, col;
+};
+
+// K codes and metadata of tile tk, V codes of tile tv.
 template <int BITS>
-__device__ __forceinline__ void v_load(VTileRegs<BITS>& r, const uint8_t* __restrict__ vc,
-                                       const int32_t* __restrict__ kq, int tid) {
+__device__ __forceinline__ void stage_load(StageRegs<BITS>& r, const SegA& a, int tk, int tv,
+                                           int tid) {
+  constexpr int kRow = BITS == 8 ? kHeadDim : kHeadDim / 2;
+  constexpr int vRow = BITS == 8 ? kTile : kTile / 2;
   constexpr int n = BITS == 8 ? 2 : 1;
+  const int t = tk;
+  const v4u* kc = reinterpret_cast<const v4u*>(a.kc0 + (size_t)tk * kTile * kRow);
+  const v4u* vc = reinterpret_cast<const v4u*>(a.vc0 + (size_t)tv * kHeadDim * vRow);
 #pragma unroll
-  for (int i = 0; i < n; ++i) r.v[i] = reinterpret_cast<const uint4*>(vc)[tid + i * kStageThreads];
-  r.pos = tid < kTile ? kq[tid] : 0;
+  for (int i = 0; i < n; ++i) r.k[i] = kc[tid + i * kThreads];
+#pragma unroll
+  for (int i = 0; i < n; ++i) r.v[i] = vc[tid + i * kThreads];
+  // wave 0: kq_pos; wave 1: lane 0 sK, lane 1 sV; the rest reload sV
+  // (choices uniform per wave or between two uniform addresses: no branch)
+  const int w = tid >> 6, lane = tid & 63;
+  const int32_t* pk = a.kq0 + (size_t)t * kTile + lane;
+  const int32_t* psk = reinterpret_cast<const int32_t*>(a.ks0 + t);
+  const int32_t* psv = reinterpret_cast<const int32_t*>(a.vs0 + t);
+  const int32_t* ps = (w == 1 && lane == 0) ? psk : psv;
+  r.meta = *(w == 0 ? pk : ps);
 }
 
+// int8 K: chunk q = row*8 + j goes to the swizzled slot of (row, j).  4-bit
+// K: chunk tid holds 32 channels of row tid/4, expanded to int8 (16*code)
+// and stored as two chunks.  V: f16 [128][kVPitch] in the permuted key order.
 template <int BITS>
-__device__ __forceinline__ void v_store(QBuf& b, const VTileRegs<BITS>& r, int tid) {
+__device__ __forceinline__ void stage_store(KBuf& kb, VBuf& vb, const StageRegs<BITS>& r, int tid) {
   if (BITS == 8) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int q = tid + i * kStageThreads;
+      const int q = tid + i * kThreads;
+      *reinterpret_cast<v4u*>(kb.k + kswz(q >> 3, q & 7)) = r.k[i];
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = tid + i * kThreads;
       const int d = q >> 2, kg = q & 3;   // channel d, keys kg*16 .. +16
-      const uint4 w = r.v[i];
+      const v4u w = r.v[i];
       uint32_t h[8];
       i8x4_to_h(w.x, h[0], h[1]);   // keys 0..3
       i8x4_to_h(w.y, h[2], h[3]);   // keys 4..7
       i8x4_to_h(w.z, h[4], h[5]);   // keys 8..11
       i8x4_to_h(w.w, h[6], h[7]);   // keys 12..15
-      uint8_t* dst = b.v + d * kVPitch + kg * 32;
-      *reinterpret_cast<uint4*>(dst) = make_uint4(h[0], h[1], h[4], h[5]);
-      *reinterpret_cast<uint4*>(dst + 16) = make_uint4(h[2], h[3], h[6], h[7]);
+      uint8_t* dst = vb.v + d * kVPitch + kg * 32;
+      *reinterpret_cast<v4u*>(dst) = v4u{h[0], h[1], h[4], h[5]};
+      *reinterpret_cast<v4u*>(dst + 16) = v4u{h[2], h[3], h[6], h[7]};
     }
   } else {
+    {
+      const int row = tid >> 2, j4 = tid & 3;
+      const v4u w = r.k[0];
+      uint32_t o[8];
+      i4x8_to_i8(w.x, o[0], o[1]);
+      i4x8_to_i8(w.y, o[2], o[3]);
+      i4x8_to_i8(w.z, o[4], o[5]);
+      i4x8_to_i8(w.w, o[6], o[7]);
+      *reinterpret_cast<v4u*>(kb.k + kswz(row, 2 * j4)) = v4u{o[0], o[1], o[2], o[3]};
+      *reinterpret_cast<v4u*>(kb.k + kswz(row, 2 * j4 + 1)) = v4u{o[4], o[5], o[6], o[7]};
+    }
     const int d = tid >> 1, kh = tid & 1;   // channel d, keys kh*32 .. +32 (16 B packed)
-    const uint4 w = r.v[0];
+    const v4u w = r.v[0];
     const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
     for (int g16 = 0; g16 < 2; ++g16) {
@@ -232,12 +255,13 @@ __device__ __forceinline__ void v_store(QBuf& b, const VTileRegs<BITS>& r, int t
       i8x4_to_h(bb[1], h[2], h[3]);
       i8x4_to_h(bb[2], h[4], h[5]);
       i8x4_to_h(bb[3], h[6], h[7]);
-      uint8_t* dst = b.v + d * kVPitch + (kh * 2 + g16) * 32;
-      *reinterpret_cast<uint4*>(dst) = make_uint4(h[0], h[1], h[4], h[5]);
-      *reinterpret_cast<uint4*>(dst + 16) = make_uint4(h[2], h[3], h[6], h[7]);
+      uint8_t* dst = vb.v + d * kVPitch + (kh * 2 + g16) * 32;
+      *reinterpret_cast<v4u*>(dst) = v4u{h[0], h[1], h[4], h[5]};
+      *reinterpret_cast<v4u*>(dst + 16) = v4u{h[2], h[3], h[6], h[7]};
     }
   }
-  if (tid < kTile) b.pos[tid] = r.pos;
+  const int w = tid >> 6, lane = tid & 63;
+  kb.pos[w == 0 ? lane : (w == 1 ? min(kMetaSK + lane, kMetaSink) : kMetaSink)] = r.meta;
 }
 
 // Stage full-precision tile: entries e0 .. e0+63 of the list
@@ -317,166 +341,128 @@ __device__ __forceinline__ void apply_corr(NState& ns) {
   ns.corr = 1.0f;
 }
 
-// Softmax of one 32-query block on one quantized tile: int32 logits s[2]
-// (two 32-key halves) -> f16 weights p[4] (the B operands of the four 16-key
-// P V steps), updating m and l.
-__device__ __forceinline__ void softmax_q(NState& ns, const v16i (&s)[2], v8h (&p)[4], float cqk,
-                                          float f, bool diag, const int32_t* pos, int tq,
-                                          int half) {
-  if (!diag && f >= 6.103515625e-05f) {
-    // fast path: every key visible; the f16 weights carry the V scale
-    int mi = s[0][0];
+// General path: causal mask by original position, tiny V scales, or a tile
+// whose maximum outgrew the reference max.  Raises m to the masked tile
+// maximum when needed and rescales l and the accumulator at once (the
+// accumulator already holds every P V product of earlier tiles).  No
+// per-lane branches, so the cross-lane swap sees every lane's operand; the
+// visibility test is evaluated twice rather than kept in registers.
+__device__ __forceinline__ void softmax_general(NState& ns, const v16i (&s)[2], v8h (&p)[4],
+                                             float cqk, float f, bool diag, const int32_t* pos,
+                                             int tq, int half) {
+  int mi = INT_MIN;
 #pragma unroll
-    for (int kh = 0; kh < 2; ++kh)
+  for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
-      for (int r = (kh == 0 ? 1 : 0); r < 16; r += 2) {
-        if (r + 1 < 16) mi = max(mi, max(s[kh][r], s[kh][r + 1]));
-        else mi = max(mi, s[kh][r]);
-      }
-    mi = xhalf_max_i(mi);
-    lazy_max(ns, (float)mi * cqk);
-    const float bias = __builtin_amdgcn_logf(f) - ns.m;   // log2
-    float ps = 0.0f;
-    const v2h one2 = {(_Float16)1.0f, (_Float16)1.0f};
+    for (int r = 0; r < 16; ++r) {
+      const bool vis = (!diag) | (pos[key_of(kh, r, half)] <= tq);
+      mi = max(mi, vis ? s[kh][r] : INT_MIN);
+    }
+  mi = xhalf_max_i(mi);
+  lazy_max(ns, mi == INT_MIN ? -INFINITY : (float)mi * cqk);
+  apply_corr(ns);
+  // The row sum adds the same f16 weights the MFMA uses (divided by f),
+  // unless f is so small that they lose precision; then the float32 ones.
+  const bool f_ok = f >= 6.103515625e-05f;
+  float ps = 0.0f;
 #pragma unroll
-    for (int kh = 0; kh < 2; ++kh)
+  for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
-      for (int r = 0; r < 16; r += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf((float)s[kh][r], cqk, bias));
-        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf((float)s[kh][r + 1], cqk, bias));
-        v2h pk;
-        pk[0] = (_Float16)p0;
-        pk[1] = (_Float16)p1;
-        ps = __builtin_amdgcn_fdot2(pk, one2, ps, false);
-        p[kh * 2 + (r >> 3)][r & 7] = pk[0];
-        p[kh * 2 + (r >> 3)][(r & 7) + 1] = pk[1];
-      }
-    ns.l = __builtin_fmaf(ps, __builtin_amdgcn_rcpf(f), ns.l);   // 1-ulp reciprocal
-  } else {
-    // general path: causal mask by original position, tiny V scales.  No
-    // per-lane branches, so the cross-lane swap sees every lane's operand;
-    // the visibility test is evaluated twice rather than kept in registers.
-    int mi = INT_MIN;
-#pragma unroll
-    for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const bool vis = (!diag) | (pos[key_of(kh, r, half)] <= tq);
-        mi = max(mi, vis ? s[kh][r] : INT_MIN);
-      }
-    mi = xhalf_max_i(mi);
-    lazy_max(ns, mi == INT_MIN ? -INFINITY : (float)mi * cqk);
-    // The row sum adds the same f16 weights the MFMA uses (divided by f),
-    // unless f is so small that they lose precision; then the float32 ones.
-    const bool f_ok = f >= 6.103515625e-05f;
-    float ps = 0.0f;
-#pragma unroll
-    for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const bool vis = (!diag) | (pos[key_of(kh, r, half)] <= tq);
-        const float ex = __builtin_amdgcn_exp2f((float)s[kh][r] * cqk - ns.m);
-        const float e = vis ? ex : 0.0f;
-        const _Float16 hp = (_Float16)(e * f);
-        ps += f_ok ? (float)hp : e;
-        p[kh * 2 + (r >> 3)][r & 7] = hp;
-      }
-    ns.l += f_ok ? ps * __builtin_amdgcn_rcpf(f) : ps;
-  }
+    for (int r = 0; r < 16; ++r) {
+      const bool vis = (!diag) | (pos[key_of(kh, r, half)] <= tq);
+      const float ex = __builtin_amdgcn_exp2f((float)s[kh][r] * cqk - ns.m);
+      const float e = vis ? ex : 0.0f;
+      const _Float16 hp = (_Float16)(e * f);
+      ps += f_ok ? (float)hp : e;
+      p[kh * 2 + (r >> 3)][r & 7] = hp;
+    }
+  ns.l += f_ok ? ps * __builtin_amdgcn_rcpf(f) : ps;
 }
 
-// Everything one wave needs for the quantized segment.
-struct SegA {
-  const uint8_t* kc0;
-  const uint8_t* vc0;
-  const int32_t* kq0;
-  const float* ks0;
-  const float* vs0;
-  int n;              // quantized tiles to scan
-  int t0;             // first query row of the wave
-  float cq;           // alpha * log2(e) * s_Q
-  float inv_vref;
-  int lane, half, col, w;
-};
-
-// One tile of the quantized segment: stage tile c+1, S^T of tile c, P V of
-// tile c-1 (weights pprev; zeros when c = 0), softmax of tile c -> pcur.
-template <int BITS, int NB>
-__device__ __forceinline__ void segA_tile(Smem& sm, const SegA& a, int c, const v4i (&qf)[NB][4],
-                                          NState (&st)[NB], const v8h (&pprev)[NB][4],
-                                          v8h (&pcur)[NB][4], VTileRegs<BITS>& vr, uint4& k4r) {
-  constexpr int kRow = BITS == 8 ? kHeadDim : kHeadDim / 2;
-  constexpr int vRow = BITS == 8 ? kTile : kTile / 2;
+// One tile of the quantized segment:
+//   publish tile c+1 (registers -> LDS) and load tile c+2 into registers;
+//   S^T of tile c (int8 MFMA);
+//   P V of tile c-1 (weights pprev; zeros when c = 0) interleaved with the
+//   fast-path softmax of tile c -> pcur;
+//   the general path instead when the tile touches the diagonal, its V
+//   scale ratio is tiny, or some weight overflowed the fast-path bound.
+// The accumulator never carries a pending rescale between tiles: only the
+// general path moves the reference max, and it rescales on the spot.
+// PH = c % 2 is a template argument so that every LDS address is a per-lane
+// constant plus an immediate offset.
+template <int BITS, int PH>
+__device__ __forceinline__ void segA_tile(Smem& sm, const SegA& a, int c, const v4i (&qf)[4],
+                                          NState& st, const v8h (&pprev)[4], v8h (&pcur)[4],
+                                          StageRegs<BITS>& sr) {
   constexpr float kSub = BITS == 8 ? 1.0f : 0.0625f;   // 4-bit codes are staged as 16*code
   const int tid = threadIdx.x;
-  const bool more = c + 1 < a.n;
-  // stage tile c+1 into the ring (its previous tile, c-2, is no longer read)
-  if (more) {
-    const uint8_t* kn = a.kc0 + (size_t)(c + 1) * kTile * kRow;
-    if (BITS == 8) k_direct_issue(sm.q[(c + 1) % kNBuf].k, kn, a.w, a.lane);
-    else k4r = k4_load(kn, tid);
-    v_load<BITS>(vr, a.vc0 + (size_t)(c + 1) * kHeadDim * vRow, a.kq0 + (size_t)(c + 1) * kTile,
-                 tid);
-  }
-  const float sk = a.ks0[c] * kSub;
-  const float sv = a.vs0[c] * kSub;
-  const QBuf& cur = sm.q[c % kNBuf];
-  const QBuf& prv = sm.q[c >= 1 ? (c - 1) % kNBuf : 0];
+  const KBuf& cur = sm.q.kb[PH];
+  const VBuf& prv = sm.q.vb[PH ^ 1];
+  const float sk = __int_as_float(cur.pos[kMetaSK]) * kSub;
+  const float sv = __int_as_float(cur.pos[kMetaSV]) * kSub;
+  const int last = __builtin_amdgcn_readfirstlane(cur.pos[kTile - 1]);
 
-  // pending accumulator rescales (from the softmax of tile c-1)
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) apply_corr(st[nb]);
-
-  // S^T of tile c: each K fragment serves every query block
+  // S^T of tile c
   v4i ka[2][4];
 #pragma unroll
   for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
     for (int k4 = 0; k4 < 4; ++k4)
       ka[kh][k4] = *reinterpret_cast<const v4i*>(cur.k + kswz(kh * 32 + a.col, k4 * 2 + a.half));
-  v16i s[NB][2];
+  v16i s[2];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
+  for (int kh = 0; kh < 2; ++kh) {
+    s[kh] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
-    for (int kh = 0; kh < 2; ++kh) {
-      s[nb][kh] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-      for (int k4 = 0; k4 < 4; ++k4)
-        s[nb][kh] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ka[kh][k4], qf[nb][k4], s[nb][kh], 0, 0, 0);
-    }
-  // P V of tile c-1: each V fragment serves every query block
-#pragma unroll
-  for (int dg = 0; dg < 4; ++dg)
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const v8h va = *reinterpret_cast<const v8h*>(prv.v + (dg * 32 + a.col) * kVPitch + ks * 32 +
-                                                   a.half * 16);
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        st[nb].acc[dg] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, pprev[nb][ks], st[nb].acc[dg], 0, 0, 0);
-    }
-  // softmax of tile c (independent of the P V products above)
+    for (int k4 = 0; k4 < 4; ++k4)
+      s[kh] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ka[kh][k4], qf[k4], s[kh], 0, 0, 0);
+  }
+  // publish K(c+1) and V(c) (registers loaded during tile c-1) and load K(c+2)
+  // and V(c+1); the conversion runs in the shadow of the MFMAs above.  Past
+  // the end the last tile is staged again into the free buffers (no branch).
+  stage_store<BITS>(sm.q.kb[PH ^ 1], sm.q.vb[PH], sr, tid);
+  stage_load<BITS>(sr, a, min(c + 2, a.n - 1), min(c + 1, a.n - 1), tid);
+
+  // Fast path: weights against the current reference max, without the tile
+  // max; accepted unless some lane's weights sum above kFastMax (then some
+  // weight may have left the f16 range).  Step i issues the MFMA of
+  // (channel group i%4, key group i/4) of P V(c-1) and the weight pair i.
   const float cqk = a.cq * sk;
   const float f = sv * a.inv_vref;
-  const int last = __builtin_amdgcn_readfirstlane(cur.pos[kTile - 1]);
+  const float bias = __builtin_amdgcn_logf(f) - st.m;   // log2
+  const v2h one2 = {(_Float16)1.0f, (_Float16)1.0f};
+  float ps = 0.0f;
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int tq = a.t0 + nb * 32 + a.col;
-    softmax_q(st[nb], s[nb], pcur[nb], cqk, f, last > a.t0 + nb * 32, cur.pos, tq, a.half);
+  for (int i = 0; i < 16; ++i) {
+    const int dg = i & 3, ks = i >> 2;
+    const v8h va = *reinterpret_cast<const v8h*>(prv.v + (dg * 32 + a.col) * kVPitch + ks * 32 +
+                                                 a.half * 16);
+    st.acc[dg] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, pprev[ks], st.acc[dg], 0, 0, 0);
+    const int kh = i >> 3, r = (i & 7) * 2;
+    const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf((float)s[kh][r], cqk, bias));
+    const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf((float)s[kh][r + 1], cqk, bias));
+    v2h pk;
+    pk[0] = (_Float16)p0;
+    pk[1] = (_Float16)p1;
+    ps = __builtin_amdgcn_fdot2(pk, one2, ps, false);
+    pcur[kh * 2 + (r >> 3)][r & 7] = pk[0];
+    pcur[kh * 2 + (r >> 3)][(r & 7) + 1] = pk[1];
   }
-  if (more) {
-    // after the math, so that the wait for memory comes last
-    __builtin_amdgcn_sched_barrier(0);
-    asm volatile("" ::: "memory");
-    if (BITS == 4) k4_store(sm.q[(c + 1) % kNBuf].k, k4r, tid);
-    v_store<BITS>(sm.q[(c + 1) % kNBuf], vr, tid);
-    __builtin_amdgcn_s_waitcnt(0);   // direct K loads complete
+  // keep the fast-path weights computed here, next to the MFMAs, rather
+  // than sunk into the branch below that consumes them
+  asm volatile("" : "+v"(pcur[0]), "+v"(pcur[1]), "+v"(pcur[2]), "+v"(pcur[3]), "+v"(ps));
+  const bool diag = last > a.t0;
+  const bool redo = diag || !(f >= 6.103515625e-05f) || __ballot(!(ps <= kFastMax)) != 0;
+  if (redo) {
+    softmax_general(st, s, pcur, cqk, f, diag, cur.pos, a.t0 + a.col, a.half);
+  } else {
+    st.l = __builtin_fmaf(ps, __builtin_amdgcn_rcpf(f), st.l);   // 1-ulp reciprocal
   }
   __syncthreads();
 }
 
-template <int BITS, int OUT_BF16, int NB>
-__global__ void __launch_bounds__(kThreads, NB == 1 ? 2 : 1)
+template <int BITS, int OUT_BF16>
+__global__ void __launch_bounds__(kThreads, 2)
 attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                     const uint16_t* __restrict__ V, const int32_t* __restrict__ idx,
                     const int8_t* __restrict__ q_codes, const float* __restrict__ q_scale,
@@ -491,9 +477,9 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
   const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int half = lane >> 5, col = lane & 31;
 
-  // Work units of one KV head: (block rb of 32*NB rows, query head hh of the
+  // Work units of one KV head: (block rb of 32 rows, query head hh of the
   // group), ordered by rb; a workgroup takes 4 consecutive units, longest first.
-  constexpr int kRows = 32 * NB;
+  constexpr int kRows = 32;
   const int nrb = (L + kRows - 1) / kRows;
   const int units = g * nrb;
   const int wg_per_bj = (units + kWaves - 1) / kWaves;
@@ -508,22 +494,21 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
   const int b = bj / Hkv, j = bj % Hkv, h = j * g + hh;
   const size_t bh = (size_t)b * Hq + h;
   const int t0 = rb * kRows;
+  const int tq = t0 + col;                 // this lane's query row
+  const bool row_ok = active && tq < L;
 
   const uint16_t* Kh = K + (size_t)bj * L * kHeadDim;
   const uint16_t* Vh = V + (size_t)bj * L * kHeadDim;
   const int32_t* vl = idx + (size_t)bj * k;
 
-  NState st[NB];
+  NState st;
+  st.m = kMinusBig;
+  st.l = 0.0f;
+  st.corr = 1.0f;
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    st[nb].m = kMinusBig;
-    st[nb].l = 0.0f;
-    st[nb].corr = 1.0f;
+  for (int dg = 0; dg < 4; ++dg)
 #pragma unroll
-    for (int dg = 0; dg < 4; ++dg)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) st[nb].acc[dg][r] = 0.0f;
-  }
+    for (int r = 0; r < 16; ++r) st.acc[dg][r] = 0.0f;
 
   // Which keys are visible to rows up to t_last.
   int nvl, nq_tiles, fp_count, fp_base;
@@ -572,78 +557,60 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
     a.lane = lane;
     a.half = half;
     a.col = col;
-    a.w = w;
 
-    v4i qf[NB][4];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int tq = t0 + nb * 32 + col;
-      const bool ok = active && tq < L;
-      const int8_t* qrow = q_codes + (bh * L + (ok ? tq : 0)) * kHeadDim;
+    v4i qf[4];
+    {
+      const int8_t* qrow = q_codes + (bh * L + (row_ok ? tq : 0)) * kHeadDim;
 #pragma unroll
       for (int k4 = 0; k4 < 4; ++k4)
-        qf[nb][k4] = ok ? *reinterpret_cast<const v4i*>(qrow + k4 * 32 + half * 16) : v4i{0, 0, 0, 0};
+        qf[k4] = row_ok ? *reinterpret_cast<const v4i*>(qrow + k4 * 32 + half * 16) : v4i{0, 0, 0, 0};
     }
 
-    // prologue: tile 0
-    VTileRegs<BITS> vr;
-    uint4 k4r = make_uint4(0, 0, 0, 0);
-    if (BITS == 8) {
-      k_direct_issue(sm.q[0].k, a.kc0, w, lane);
-    } else {
-      k4r = k4_load(a.kc0, threadIdx.x);
-      k4_store(sm.q[0].k, k4r, threadIdx.x);
-    }
-    v_load<BITS>(vr, a.vc0, a.kq0, threadIdx.x);
-    v_store<BITS>(sm.q[0], vr, threadIdx.x);
-    __builtin_amdgcn_s_waitcnt(0);
+    // prologue: K(0) into LDS, K(1) and V(0) into registers; the V buffer
+    // that tile 0 multiplies by zero weights is cleared (no stale NaNs)
+    StageRegs<BITS> sr;
+    stage_load<BITS>(sr, a, 0, 0, threadIdx.x);
+    stage_store<BITS>(sm.q.kb[0], sm.q.vb[1], sr, threadIdx.x);
+    stage_load<BITS>(sr, a, min(1, nq_tiles - 1), 0, threadIdx.x);
+    __syncthreads();
+    for (int i = threadIdx.x; i < kVBytes / 16; i += kThreads)
+      reinterpret_cast<v4u*>(sm.q.vb[1].v)[i] = v4u{0u, 0u, 0u, 0u};
     __syncthreads();
 
     // the P V of tile c runs in iteration c+1, next to the softmax of c+1;
     // the weights alternate between two register sets
-    v8h pa[NB][4], pb[NB][4];
+    v8h pa[4], pb[4];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) pa[nb][i][e] = pb[nb][i][e] = (_Float16)0.0f;
+      for (int e = 0; e < 8; ++e) pa[i][e] = pb[i][e] = (_Float16)0.0f;
     int c = 0;
     for (; c + 1 < nq_tiles; c += 2) {
-      segA_tile<BITS, NB>(sm, a, c, qf, st, pa, pb, vr, k4r);
-      segA_tile<BITS, NB>(sm, a, c + 1, qf, st, pb, pa, vr, k4r);
+      segA_tile<BITS, 0>(sm, a, c, qf, st, pa, pb, sr);
+      segA_tile<BITS, 1>(sm, a, c + 1, qf, st, pb, pa, sr);
     }
-    if (c < nq_tiles) {
-      segA_tile<BITS, NB>(sm, a, c, qf, st, pa, pb, vr, k4r);
-      ++c;
-    }
+    if (c < nq_tiles) segA_tile<BITS, 0>(sm, a, c, qf, st, pa, pb, sr);
     // P V of the last tile
-    const v8h (&plast)[NB][4] = (nq_tiles & 1) ? pb : pa;
-    const QBuf& lb = sm.q[(nq_tiles - 1) % kNBuf];
+    const v8h (&plast)[4] = (nq_tiles & 1) ? pb : pa;
+    const VBuf& lb = sm.q.vb[(nq_tiles - 1) & 1];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) apply_corr(st[nb]);
+    for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-    for (int dg = 0; dg < 4; ++dg)
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
+      for (int dg = 0; dg < 4; ++dg) {
         const v8h va = *reinterpret_cast<const v8h*>(lb.v + (dg * 32 + col) * kVPitch + ks * 32 +
                                                      half * 16);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          st[nb].acc[dg] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, plast[nb][ks], st[nb].acc[dg], 0, 0, 0);
+        st.acc[dg] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, plast[ks], st.acc[dg], 0, 0, 0);
       }
     __syncthreads();   // the FP segment reuses the LDS
   }
 
   // ---------------- segments B and C: full-precision keys ----------------
   if (fp_count > 0) {
-    v8bf qb[NB][8];
+    v8bf qb[8];
+    {
+      const uint16_t* qrow = Q + (bh * L + (row_ok ? tq : 0)) * kHeadDim;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int tq = t0 + nb * 32 + col;
-      const uint16_t* qrow = Q + (bh * L + ((active && tq < L) ? tq : 0)) * kHeadDim;
-#pragma unroll
-      for (int ks = 0; ks < 8; ++ks) qb[nb][ks] = *reinterpret_cast<const v8bf*>(qrow + ks * 16 + half * 8);
+      for (int ks = 0; ks < 8; ++ks) qb[ks] = *reinterpret_cast<const v8bf*>(qrow + ks * 16 + half * 8);
     }
     const int nft = (fp_count + kTile - 1) / kTile;
     FBuf& fb = sm.f;
@@ -658,90 +625,79 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
         for (int ks = 0; ks < 8; ++ks)
           ka[kh][ks] = *reinterpret_cast<const v8bf*>(fb.k + (kh * 32 + col) * kKPitchBf + ks * 32 +
                                                       half * 16);
-      v8bf phi[NB][4], plo[NB][4];
+      v8bf phi[4], plo[4];
+      v16f sf[2];
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int tq = t0 + nb * 32 + col;
-        v16f sf[2];
+      for (int kh = 0; kh < 2; ++kh) {
 #pragma unroll
-        for (int kh = 0; kh < 2; ++kh) {
+        for (int r = 0; r < 16; ++r) sf[kh][r] = 0.0f;
 #pragma unroll
-          for (int r = 0; r < 16; ++r) sf[kh][r] = 0.0f;
-#pragma unroll
-          for (int ks = 0; ks < 8; ++ks)
-            sf[kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[kh][ks], qb[nb][ks], sf[kh], 0, 0, 0);
-        }
-        float mt = -INFINITY;
-#pragma unroll
-        for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const bool vis = fb.pos[key_of(kh, r, half)] <= tq;
-            mt = fmaxf(mt, vis ? sf[kh][r] * alpha_log2e : -INFINITY);
-          }
-        lazy_max(st[nb], xhalf_max(mt));
-        apply_corr(st[nb]);
-        float ps = 0.0f;
-#pragma unroll
-        for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const bool vis = fb.pos[key_of(kh, r, half)] <= tq;
-            const float ex = __builtin_amdgcn_exp2f(sf[kh][r] * alpha_log2e - st[nb].m);
-            const float pv = vis ? ex : 0.0f;
-            ps += pv;
-            const float pp = pv * inv_vref;
-            const __bf16 hi = (__bf16)pp;
-            const __bf16 lo = (__bf16)(pp - (float)hi);
-            phi[nb][kh * 2 + (r >> 3)][r & 7] = hi;
-            plo[nb][kh * 2 + (r >> 3)][r & 7] = lo;
-          }
-        st[nb].l += ps;
+        for (int ks = 0; ks < 8; ++ks)
+          sf[kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[kh][ks], qb[ks], sf[kh], 0, 0, 0);
       }
+      float mt = -INFINITY;
+#pragma unroll
+      for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const bool vis = fb.pos[key_of(kh, r, half)] <= tq;
+          mt = fmaxf(mt, vis ? sf[kh][r] * alpha_log2e : -INFINITY);
+        }
+      lazy_max(st, xhalf_max(mt));
+      apply_corr(st);
+      float ps = 0.0f;
+#pragma unroll
+      for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const bool vis = fb.pos[key_of(kh, r, half)] <= tq;
+          const float ex = __builtin_amdgcn_exp2f(sf[kh][r] * alpha_log2e - st.m);
+          const float pv = vis ? ex : 0.0f;
+          ps += pv;
+          const float pp = pv * inv_vref;
+          const __bf16 hi = (__bf16)pp;
+          const __bf16 lo = (__bf16)(pp - (float)hi);
+          phi[kh * 2 + (r >> 3)][r & 7] = hi;
+          plo[kh * 2 + (r >> 3)][r & 7] = lo;
+        }
+      st.l += ps;
 #pragma unroll
       for (int dg = 0; dg < 4; ++dg)
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
           const v8bf va = *reinterpret_cast<const v8bf*>(fb.v + (dg * 32 + col) * kVPitch + ks * 32 +
                                                          half * 16);
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) {
-            st[nb].acc[dg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, phi[nb][ks], st[nb].acc[dg], 0, 0, 0);
-            st[nb].acc[dg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, plo[nb][ks], st[nb].acc[dg], 0, 0, 0);
-          }
+          st.acc[dg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, phi[ks], st.acc[dg], 0, 0, 0);
+          st.acc[dg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, plo[ks], st.acc[dg], 0, 0, 0);
         }
     }
   }
 
   // ---------------- finalize: O = acc * sVref / l ----------------
+  const float ltot = xhalf_sum(st.l);
+  const float sc = vref / ltot;
+  if (!row_ok) return;
+  const size_t obase = (bh * L + tq) * kHeadDim;
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const float ltot = xhalf_sum(st[nb].l);
-    const float sc = vref / ltot;
-    const int tq = t0 + nb * 32 + col;
-    if (!(active && tq < L)) continue;
-    const size_t obase = (bh * L + tq) * kHeadDim;
+  for (int dg = 0; dg < 4; ++dg)
 #pragma unroll
-    for (int dg = 0; dg < 4; ++dg)
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const int d = dg * 32 + r4 * 8 + half * 4;
-        const float o0 = st[nb].acc[dg][r4 * 4 + 0] * sc, o1 = st[nb].acc[dg][r4 * 4 + 1] * sc;
-        const float o2 = st[nb].acc[dg][r4 * 4 + 2] * sc, o3 = st[nb].acc[dg][r4 * 4 + 3] * sc;
-        if (OUT_BF16) {
-          uint16_t* o = reinterpret_cast<uint16_t*>(out) + obase + d;
-          const __bf16 b0 = (__bf16)o0, b1 = (__bf16)o1, b2 = (__bf16)o2, b3 = (__bf16)o3;
-          const uint32_t w0 = (uint32_t)__builtin_bit_cast(uint16_t, b0) |
-                              ((uint32_t)__builtin_bit_cast(uint16_t, b1) << 16);
-          const uint32_t w1 = (uint32_t)__builtin_bit_cast(uint16_t, b2) |
-                              ((uint32_t)__builtin_bit_cast(uint16_t, b3) << 16);
-          *reinterpret_cast<uint2*>(o) = make_uint2(w0, w1);
-        } else {
-          float* o = reinterpret_cast<float*>(out) + obase + d;
-          *reinterpret_cast<float4*>(o) = make_float4(o0, o1, o2, o3);
-        }
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int d = dg * 32 + r4 * 8 + half * 4;
+      const float o0 = st.acc[dg][r4 * 4 + 0] * sc, o1 = st.acc[dg][r4 * 4 + 1] * sc;
+      const float o2 = st.acc[dg][r4 * 4 + 2] * sc, o3 = st.acc[dg][r4 * 4 + 3] * sc;
+      if (OUT_BF16) {
+        uint16_t* o = reinterpret_cast<uint16_t*>(out) + obase + d;
+        const __bf16 b0 = (__bf16)o0, b1 = (__bf16)o1, b2 = (__bf16)o2, b3 = (__bf16)o3;
+        const uint32_t w0 = (uint32_t)__builtin_bit_cast(uint16_t, b0) |
+                            ((uint32_t)__builtin_bit_cast(uint16_t, b1) << 16);
+        const uint32_t w1 = (uint32_t)__builtin_bit_cast(uint16_t, b2) |
+                            ((uint32_t)__builtin_bit_cast(uint16_t, b3) << 16);
+        *reinterpret_cast<uint2*>(o) = make_uint2(w0, w1);
+      } else {
+        float* o = reinterpret_cast<float*>(out) + obase + d;
+        *reinterpret_cast<float4*>(o) = make_float4(o0, o1, o2, o3);
       }
-  }
+    }
 }
 
 template <int BITS, int OB>
@@ -751,11 +707,11 @@ hipError_t launch_t(const hyq_shape& s, const hyq_sizes& z, const uint16_t* Q,
                     const float* k_scale, const uint8_t* v_codes, const float* v_scale,
                     const int32_t* kq_pos, float softmax_scale, void* out, hipStream_t st) {
   const int g = s.Hq / s.Hkv;
-  const int nrb = (s.L + 32 * kNB - 1) / (32 * kNB);
+  const int nrb = (s.L + 31) / 32;
   const int wg_per_bj = (g * nrb + kWaves - 1) / kWaves;
   const int nbj = s.B * s.Hkv;
   const dim3 grid(wg_per_bj * nbj);
-  attn_prefill_kernel<BITS, OB, kNB><<<grid, kThreads, 0, st>>>(
+  attn_prefill_kernel<BITS, OB><<<grid, kThreads, 0, st>>>(
       Q, K, V, idx, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, kq_pos, out, s.Hq,
       s.Hkv, nbj, s.L, z.P, z.k, z.nQ, z.n_qblk, z.n_kvblk, softmax_scale * kLog2e);
   return hipGetLastError();
