@@ -113,6 +113,9 @@ def main():
     ap.add_argument("--cpu-budget-s", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--traffic-probe", action="store_true",
+                    help="for rocprofv3 --pmc runs: one step, a plain 1 GiB copy kernel of known "
+                         "traffic (the counter scale), one more step; no timing")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -164,6 +167,20 @@ def main():
                              bufs["kq_pos"], scale, bufs["out"], out_dtype, stream)
         if ev:
             ev[3].record(stream)
+
+    if args.traffic_probe:
+        step()
+        n = 1 << 28   # float32 elements: 1 GiB read + 1 GiB written
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        step()
+        torch.cuda.synchronize()
+        print(f"[bench] traffic probe done: copy kernel reads and writes {4 * n} bytes",
+              file=sys.stderr, flush=True)
+        return
 
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
