@@ -113,6 +113,11 @@ def main():
     ap.add_argument("--cpu-budget-s", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--hq", type=int, default=None,
+                    help="keep only the first HQ query heads (with their KV heads): e.g. --hq 4 "
+                         "is one GPU's share of config 3 under 8-way head sharding")
+    ap.add_argument("--no-bits16", action="store_true",
+                    help="skip the full-precision (bits 16) attention of the same inputs")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for rocprofv3 --pmc runs: one step, a plain 1 GiB copy kernel of known "
                          "traffic (the counter scale), one more step; no timing")
@@ -142,7 +147,19 @@ def main():
     def t(x):
         return torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev)
 
-    Q, K, V = t(d["Q"]), t(d["K"]), t(d["V"])
+    if args.hq is not None:
+        g = cfg["Hq"] // cfg["Hkv"]
+        if args.hq % g or not 0 < args.hq <= cfg["Hq"]:
+            print(f"--hq must be a multiple of the group size {g} and at most {cfg['Hq']}",
+                  file=sys.stderr)
+            sys.exit(2)
+        hkv = args.hq // g
+        d["Q"], d["K"], d["V"] = d["Q"][:, :args.hq], d["K"][:, :hkv], d["V"][:, :hkv]
+        d["planted"] = [d["planted"][b * cfg["Hkv"] + j] for b in range(cfg["B"])
+                        for j in range(hkv)]
+        cfg["Hq"], cfg["Hkv"] = args.hq, hkv
+    Q, K, V = t(np.ascontiguousarray(d["Q"])), t(np.ascontiguousarray(d["K"])), \
+        t(np.ascontiguousarray(d["V"]))
     shape = hyq.Shape(B=cfg["B"], Hq=cfg["Hq"], Hkv=cfg["Hkv"], L=cfg["L"], window=cfg["W"],
                       budget_ppm=cfg["budget_ppm"], bits_kv=cfg["bits"])
     out_dtype = 1 if args.out_bf16 else 0
@@ -200,6 +217,35 @@ def main():
     att = [e[2].elapsed_time(e[3]) for e in evs]
     attn_ms = float(np.mean(att))
 
+    # the same inputs through our own kernel with every key in full precision
+    # (bits 16): the in-house exact-attention comparison
+    bits16 = None
+    if not args.no_bits16 and shape.bits_kv != 16:
+        s16 = hyq.Shape(B=shape.B, Hq=shape.Hq, Hkv=shape.Hkv, L=shape.L, window=shape.window,
+                        budget_ppm=shape.budget_ppm, bits_kv=16)
+        b16 = hyq.alloc_buffers(s16, dev, out_dtype)
+        print("[bench] bits-16 attention", file=sys.stderr, flush=True)
+
+        def step16():
+            hyq.hyq_attn_prefill(s16, Q, K, V, b16["idx"], b16["q_codes"], b16["q_scale"],
+                                 b16["k_codes"], b16["k_scale"], b16["v_codes"], b16["v_scale"],
+                                 b16["kq_pos"], scale, b16["out"], out_dtype, stream)
+        step16()
+        torch.cuda.synchronize()
+        e16 = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(5)]
+        for e in e16:
+            e[0].record(stream)
+            step16()
+            e[1].record(stream)
+        torch.cuda.synchronize()
+        ms16 = float(np.median([e[0].elapsed_time(e[1]) for e in e16]))
+        bits16 = {"attention_ms_median": round(ms16, 4),
+                  "tflops": round(causal_flops(shape.B, shape.Hq, shape.L, shape.D) /
+                                  (ms16 * 1e-3) / 1e12, 2),
+                  "speedup_of_hybrid": round(ms16 / float(np.median(att)), 3)}
+        del b16
+
     flops = causal_flops(shape.B, shape.Hq, shape.L, shape.D)
     value = flops / (ms_step * 1e-3) / 1e12
     attn_tflops = flops / (attn_ms * 1e-3) / 1e12
@@ -246,6 +292,10 @@ def main():
         "ms_per_layer": {"total": round(ms_step, 4), "attention": round(attn_ms, 4),
                          "select": round(float(np.mean(sel)), 4),
                          "quantize": round(float(np.mean(qnt)), 4)},
+        "ms_median": {"attention": round(float(np.median(att)), 4),
+                      "select": round(float(np.median(sel)), 4),
+                      "quantize": round(float(np.median(qnt)), 4)},
+        "bits16_same_inputs": bits16,
         "attention_tflops": round(attn_tflops, 2),
         "frac_int8_peak": round(attn_tflops / INT8_PEAK_TOPS, 4),
         "frac_blended_ceiling": round(attn_tflops / BLENDED_PEAK, 4),

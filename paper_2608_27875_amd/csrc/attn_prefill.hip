@@ -60,8 +60,9 @@ constexpr float kMinusBig = -1.0e30f;
 // LDS row pitches (bytes).  +16 keeps the 16-byte reads of 8 consecutive
 // rows on distinct banks.
 // int8 K tile: 64 rows of 128 B with no padding; the 16-byte chunk j of row r
-// is stored at slot j ^ (r % 8), which keeps 16-byte reads of 8 consecutive
-// rows on distinct banks.
+// is stored at slot j ^ ((r / 2) % 8): a 256-byte bank row holds two K rows,
+// so the 16 lanes of one 16-byte read phase (16 consecutive rows, one chunk)
+// land on distinct banks.
 constexpr int kKRowI8 = kHeadDim;
 constexpr int kKPitchBf = kHeadDim * 2 + 16;    // bf16 K row
 constexpr int kVPitch = kTile * 2 + 16;          // one channel of 64 f16/bf16 keys
@@ -79,10 +80,13 @@ struct KBuf {                       // K codes and metadata of one quantized til
 struct VBuf {                       // V of one quantized tile as f16 V^T
   alignas(16) uint8_t v[kVBytes];
 };
-// Quantized segment: tile c reads K(c) from kb[c%2] and V(c-1) from
-// vb[(c-1)%2] while K(c+1) is written to kb[(c+1)%2] and V(c) to vb[c%2].
+// Quantized segment: tile c multiplies K(c) (fragments read from kb[c%4] at
+// the end of tile c-1) and V(c-1) from vb[(c-1)%2]; it writes K(c+2) to
+// kb[(c+2)%4] and V(c) to vb[c%2], and reads the fragments of K(c+1) from
+// kb[(c+1)%4] (published one barrier earlier) before its closing barrier.
+constexpr int kKRing = 4;
 struct QRing {
-  KBuf kb[2];
+  KBuf kb[kKRing];
   VBuf vb[2];
 };
 struct FBuf {                       // one full-precision tile
@@ -156,7 +160,7 @@ __device__ __forceinline__ int vslot(int e) {
 // codes (channel-major), kq_pos and the two block scales of one tile.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int kswz(int row, int chunk) {
-  return row * kKRowI8 + ((chunk ^ (row & 7)) << 4);
+  return row * kKRowI8 + ((chunk ^ ((row >> 1) & 7)) << 4);
 }
 
 // (native vectors: aggregate copies of HIP's uint4 would go through memory)
@@ -166,6 +170,19 @@ struct StageRegs {
   v4u v[BITS == 8 ? 2 : 1];     // same for a V tile
   int32_t meta;                 // threads 0..63: kq_pos; 64, 65: sK, sV bits (K's tile)
 };
+
+// K fragments of one tile for the S^T product (A operands, 2 halves x 4 steps).
+struct KFrag {
+  v4i f[2][4];
+};
+
+__device__ __forceinline__ void read_kfrag(KFrag& kf, const KBuf& b, int col, int half) {
+#pragma unroll
+  for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+    for (int k4 = 0; k4 < 4; ++k4)
+      kf.f[kh][k4] = *reinterpret_cast<const v4i*>(b.k + kswz(kh * 32 + col, k4 * 2 + half));
+}
 
 // Everything one wave needs for the quantized segment.
 struct SegA {
@@ -388,40 +405,34 @@ __device__ __forceinline__ void softmax_general(NState& ns, const v16i (&s)[2], 
 //   scale ratio is tiny, or some weight overflowed the fast-path bound.
 // The accumulator never carries a pending rescale between tiles: only the
 // general path moves the reference max, and it rescales on the spot.
-// PH = c % 2 is a template argument so that every LDS address is a per-lane
+// PH = c % 4 is a template argument so that every LDS address is a per-lane
 // constant plus an immediate offset.
 template <int BITS, int PH>
 __device__ __forceinline__ void segA_tile(Smem& sm, const SegA& a, int c, const v4i (&qf)[4],
                                           NState& st, const v8h (&pprev)[4], v8h (&pcur)[4],
-                                          StageRegs<BITS>& sr) {
+                                          StageRegs<BITS>& sr, KFrag& kf) {
   constexpr float kSub = BITS == 8 ? 1.0f : 0.0625f;   // 4-bit codes are staged as 16*code
   const int tid = threadIdx.x;
   const KBuf& cur = sm.q.kb[PH];
-  const VBuf& prv = sm.q.vb[PH ^ 1];
+  const VBuf& prv = sm.q.vb[(PH + 1) & 1];
   const float sk = __int_as_float(cur.pos[kMetaSK]) * kSub;
   const float sv = __int_as_float(cur.pos[kMetaSV]) * kSub;
   const int last = __builtin_amdgcn_readfirstlane(cur.pos[kTile - 1]);
 
-  // S^T of tile c
-  v4i ka[2][4];
-#pragma unroll
-  for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-    for (int k4 = 0; k4 < 4; ++k4)
-      ka[kh][k4] = *reinterpret_cast<const v4i*>(cur.k + kswz(kh * 32 + a.col, k4 * 2 + a.half));
+  // S^T of tile c (its K fragments arrived during the previous tile)
   v16i s[2];
 #pragma unroll
   for (int kh = 0; kh < 2; ++kh) {
     s[kh] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
     for (int k4 = 0; k4 < 4; ++k4)
-      s[kh] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ka[kh][k4], qf[k4], s[kh], 0, 0, 0);
+      s[kh] = __builtin_amdgcn_mfma_i32_32x32x32_i8(kf.f[kh][k4], qf[k4], s[kh], 0, 0, 0);
   }
-  // publish K(c+1) and V(c) (registers loaded during tile c-1) and load K(c+2)
+  // publish K(c+2) and V(c) (registers loaded during tile c-1) and load K(c+3)
   // and V(c+1); the conversion runs in the shadow of the MFMAs above.  Past
   // the end the last tile is staged again into the free buffers (no branch).
-  stage_store<BITS>(sm.q.kb[PH ^ 1], sm.q.vb[PH], sr, tid);
-  stage_load<BITS>(sr, a, min(c + 2, a.n - 1), min(c + 1, a.n - 1), tid);
+  stage_store<BITS>(sm.q.kb[(PH + 2) % kKRing], sm.q.vb[PH & 1], sr, tid);
+  stage_load<BITS>(sr, a, min(c + 3, a.n - 1), min(c + 1, a.n - 1), tid);
 
   // Fast path: weights against the current reference max, without the tile
   // max; accepted unless some lane's weights sum above kFastMax (then some
@@ -458,6 +469,9 @@ __device__ __forceinline__ void segA_tile(Smem& sm, const SegA& a, int c, const 
   } else {
     st.l = __builtin_fmaf(ps, __builtin_amdgcn_rcpf(f), st.l);   // 1-ulp reciprocal
   }
+  // K fragments of tile c+1 (published by the previous barrier); past the
+  // end they read a staged copy and are not used
+  read_kfrag(kf, sm.q.kb[(PH + 1) % kKRing], a.col, a.half);
   __syncthreads();
 }
 
@@ -566,15 +580,20 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
         qf[k4] = row_ok ? *reinterpret_cast<const v4i*>(qrow + k4 * 32 + half * 16) : v4i{0, 0, 0, 0};
     }
 
-    // prologue: K(0) into LDS, K(1) and V(0) into registers; the V buffer
-    // that tile 0 multiplies by zero weights is cleared (no stale NaNs)
+    // prologue: K(0), K(1) into LDS, K(2) and V(0) into registers, the
+    // fragments of K(0) read; the V buffer that tile 0 multiplies by zero
+    // weights is cleared (no stale NaNs)
     StageRegs<BITS> sr;
     stage_load<BITS>(sr, a, 0, 0, threadIdx.x);
     stage_store<BITS>(sm.q.kb[0], sm.q.vb[1], sr, threadIdx.x);
     stage_load<BITS>(sr, a, min(1, nq_tiles - 1), 0, threadIdx.x);
+    stage_store<BITS>(sm.q.kb[1], sm.q.vb[1], sr, threadIdx.x);
+    stage_load<BITS>(sr, a, min(2, nq_tiles - 1), 0, threadIdx.x);
     __syncthreads();
     for (int i = threadIdx.x; i < kVBytes / 16; i += kThreads)
       reinterpret_cast<v4u*>(sm.q.vb[1].v)[i] = v4u{0u, 0u, 0u, 0u};
+    KFrag kf;
+    read_kfrag(kf, sm.q.kb[0], col, half);
     __syncthreads();
 
     // the P V of tile c runs in iteration c+1, next to the softmax of c+1;
@@ -585,11 +604,15 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
 #pragma unroll
       for (int e = 0; e < 8; ++e) pa[i][e] = pb[i][e] = (_Float16)0.0f;
     int c = 0;
-    for (; c + 1 < nq_tiles; c += 2) {
-      segA_tile<BITS, 0>(sm, a, c, qf, st, pa, pb, sr);
-      segA_tile<BITS, 1>(sm, a, c + 1, qf, st, pb, pa, sr);
+    for (; c + 3 < nq_tiles; c += 4) {
+      segA_tile<BITS, 0>(sm, a, c, qf, st, pa, pb, sr, kf);
+      segA_tile<BITS, 1>(sm, a, c + 1, qf, st, pb, pa, sr, kf);
+      segA_tile<BITS, 2>(sm, a, c + 2, qf, st, pa, pb, sr, kf);
+      segA_tile<BITS, 3>(sm, a, c + 3, qf, st, pb, pa, sr, kf);
     }
-    if (c < nq_tiles) segA_tile<BITS, 0>(sm, a, c, qf, st, pa, pb, sr);
+    if (c < nq_tiles) segA_tile<BITS, 0>(sm, a, c, qf, st, pa, pb, sr, kf);
+    if (c + 1 < nq_tiles) segA_tile<BITS, 1>(sm, a, c + 1, qf, st, pb, pa, sr, kf);
+    if (c + 2 < nq_tiles) segA_tile<BITS, 2>(sm, a, c + 2, qf, st, pa, pb, sr, kf);
     // P V of the last tile
     const v8h (&plast)[4] = (nq_tiles & 1) ? pb : pa;
     const VBuf& lb = sm.q.vb[(nq_tiles - 1) & 1];
