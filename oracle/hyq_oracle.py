@@ -35,6 +35,11 @@ path follows the same ones):
   is fl32(amax / c) and the code rint_half_even(fl32(x / s)) clamped to
   [-c, c]; an all-zero block has scale 0 and codes 0; c = 127 for 8-bit and
   7 for 4-bit; Q is always 8-bit when K/V are quantized;
+* FP8 (Algorithm 2's second bit-width, c_B = 448): the format is OCP E4M3
+  ("e4m3fn": no infinities, largest finite 448); the code of x is the E4M3
+  value nearest to fl32(x / s), ties to the even code, saturating at +-448,
+  the sign kept when the result is zero; Q, K_Q and V_Q all use it; codes
+  are stored as their bit patterns (uint8);
 * causality holds by original key position in every segment;
 * bits = 16 disables quantization: every key takes the full-precision path.
 
@@ -56,6 +61,8 @@ import numpy as np
 
 C_INT8 = 127
 C_INT4 = 7
+C_FP8 = 448          # c_B for FP8 (Algorithm 2, Stage 2)
+FORMATS = ("int", "fp8")
 
 
 # ---------------------------------------------------------------------------
@@ -75,6 +82,55 @@ def code_bound(bits: int) -> int:
     if bits == 4:
         return C_INT4
     raise ValueError("no code bound for bits=%d" % bits)
+
+
+def e4m3_values() -> np.ndarray:
+    """Values of the 256 OCP FP8 E4M3 codes (float64): bit 7 sign, bits 6..3
+    exponent with bias 7, bits 2..0 mantissa; exponent 0 is subnormal
+    (m/8 * 2^-6); codes 0x7F and 0xFF are NaN; there are no infinities."""
+    out = np.empty(256, dtype=np.float64)
+    for code in range(256):
+        sign = -1.0 if code & 0x80 else 1.0
+        e = (code >> 3) & 0xF
+        m = code & 0x7
+        if e == 0xF and m == 0x7:
+            out[code] = np.nan
+        elif e == 0:
+            out[code] = sign * (m / 8.0) * 2.0 ** -6
+        else:
+            out[code] = sign * (1.0 + m / 8.0) * 2.0 ** (e - 7)
+    return out
+
+
+_E4M3 = e4m3_values()
+
+
+def e4m3_decode(codes: np.ndarray) -> np.ndarray:
+    """FP8 E4M3 bit patterns -> float64 values (exact)."""
+    return _E4M3[np.asarray(codes).astype(np.uint8)]
+
+
+def e4m3_encode(y: np.ndarray) -> np.ndarray:
+    """float32 -> FP8 E4M3 bit patterns: the nearest finite E4M3 value, ties
+    to the even code, |y| >= 448 saturating to +-448, the sign bit kept when
+    the result is zero (-0 for negative inputs that round to 0)."""
+    y = np.asarray(y, dtype=np.float32)
+    mags = _E4M3[:127]                         # codes 0..126: 0 .. 448, ascending
+    a = np.minimum(np.abs(y).astype(np.float64), 448.0)
+    hi = np.clip(np.searchsorted(mags, a, side="left"), 1, 126)
+    lo = hi - 1
+    dlo = a - mags[lo]
+    dhi = mags[hi] - a
+    code = np.where(dlo < dhi, lo, np.where(dhi < dlo, hi, np.where(lo % 2 == 0, lo, hi)))
+    code = code.astype(np.uint8)
+    return np.where(np.signbit(y), code | np.uint8(0x80), code).astype(np.uint8)
+
+
+def code_values(codes: np.ndarray, fmt: str) -> np.ndarray:
+    """The numbers the stored codes stand for (float64)."""
+    if fmt == "fp8":
+        return e4m3_decode(codes)
+    return np.asarray(codes).astype(np.float64)
 
 
 def sizes(L: int, W: int, budget_ppm: int, block: int = 64) -> dict:
@@ -207,14 +263,34 @@ def quantize_rows(x: np.ndarray, block: int, c: int):
     return codes.reshape(nb * block, D)[:n].astype(np.int8), scales
 
 
-def quantize(Qb, Kb, Vb, idx, W: int, bits: int, block: int = 64):
+def quantize_rows_fp8(x: np.ndarray, block: int):
+    """Per-block FP8 quantization of rows x [n, D] (float32): Algorithm 2
+    Stage 2 with c_B = 448, s = fl32(max|x| / 448), code = E4M3(fl32(x / s));
+    s = 0 gives codes 0.  Returns (codes uint8 [n, D], scales float32)."""
+    n, D = x.shape
+    nb = -(-n // block)
+    padded = np.zeros((nb * block, D), dtype=np.float32)
+    padded[:n] = x
+    blocks = padded.reshape(nb, block, D)
+    amax = np.abs(blocks).max(axis=(1, 2))
+    scales = (amax / np.float32(C_FP8)).astype(np.float32)
+    safe = np.where(scales == 0, np.float32(1.0), scales)
+    codes = e4m3_encode((blocks / safe[:, None, None]).astype(np.float32))
+    codes[scales == 0] = 0
+    return codes.reshape(nb * block, D)[:n], scales
+
+
+def quantize(Qb, Kb, Vb, idx, W: int, bits: int, block: int = 64, fmt: str = "int"):
     """Algorithm 2, Stages 1-2 on bf16 inputs.
 
-    Returns a dict: kq_pos [B,Hkv,nQ]; q_codes int8 [B,Hq,L,D], q_scale
-    [B,Hq,n_qblk]; k_codes / v_codes int8 [B,Hkv,nQ,D] (values in [-c, c],
-    not packed), k_scale / v_scale [B,Hkv,n_kvblk].  bits = 16 returns only
-    kq_pos (nothing is quantized).
+    Returns a dict: kq_pos [B,Hkv,nQ]; q_codes [B,Hq,L,D], q_scale
+    [B,Hq,n_qblk]; k_codes / v_codes [B,Hkv,nQ,D] (not packed), k_scale /
+    v_scale [B,Hkv,n_kvblk].  ``fmt`` "int": int8 codes in [-c, c]; "fp8"
+    (bits must be 8): E4M3 bit patterns (uint8) for Q, K and V.  bits = 16
+    returns only kq_pos (nothing is quantized).
     """
+    if fmt not in FORMATS or (fmt == "fp8" and bits != 8):
+        raise ValueError("fmt must be 'int', or 'fp8' with bits = 8")
     B, Hq, L, D = Qb.shape
     Hkv = Kb.shape[1]
     P = max(0, L - W)
@@ -222,26 +298,34 @@ def quantize(Qb, Kb, Vb, idx, W: int, bits: int, block: int = 64):
     out = dict(kq_pos=kq_pos)
     if bits == 16:
         return out
-    c = code_bound(bits)
     nQ = kq_pos.shape[2]
     n_qblk = -(-L // block)
     n_kvblk = -(-nQ // block)
-    q_codes = np.zeros((B, Hq, L, D), np.int8)
+    if fmt == "fp8":
+        def qrows(x, c):
+            return quantize_rows_fp8(x, block)
+        ctype = np.uint8
+    else:
+        def qrows(x, c):
+            return quantize_rows(x, block, c)
+        ctype = np.int8
+    c = code_bound(bits)
+    q_codes = np.zeros((B, Hq, L, D), ctype)
     q_scale = np.zeros((B, Hq, n_qblk), np.float32)
     for b in range(B):
         for h in range(Hq):
-            q_codes[b, h], q_scale[b, h] = quantize_rows(bf16_to_f32(Qb[b, h]), block, C_INT8)
-    k_codes = np.zeros((B, Hkv, nQ, D), np.int8)
-    v_codes = np.zeros((B, Hkv, nQ, D), np.int8)
+            q_codes[b, h], q_scale[b, h] = qrows(bf16_to_f32(Qb[b, h]), C_INT8)
+    k_codes = np.zeros((B, Hkv, nQ, D), ctype)
+    v_codes = np.zeros((B, Hkv, nQ, D), ctype)
     k_scale = np.zeros((B, Hkv, n_kvblk), np.float32)
     v_scale = np.zeros((B, Hkv, n_kvblk), np.float32)
     for b in range(B):
         for j in range(Hkv):
             rows = kq_pos[b, j]
-            k_codes[b, j], k_scale[b, j] = quantize_rows(bf16_to_f32(Kb[b, j][rows]), block, c)
-            v_codes[b, j], v_scale[b, j] = quantize_rows(bf16_to_f32(Vb[b, j][rows]), block, c)
+            k_codes[b, j], k_scale[b, j] = qrows(bf16_to_f32(Kb[b, j][rows]), c)
+            v_codes[b, j], v_scale[b, j] = qrows(bf16_to_f32(Vb[b, j][rows]), c)
     out.update(q_codes=q_codes, q_scale=q_scale, k_codes=k_codes, k_scale=k_scale,
-               v_codes=v_codes, v_scale=v_scale)
+               v_codes=v_codes, v_scale=v_scale, fmt=fmt)
     return out
 
 
@@ -269,13 +353,14 @@ def _head_operands(Qb, Kb, Vb, b, h, Hkv, W, bits, block, idx, qz):
     if bits != 16:
         nQ = qz["kq_pos"].shape[2]
         blk = np.arange(nQ) // block
+        fmt = qz.get("fmt", "int")
         ops.update(
             q_pos=qz["kq_pos"][b, j].astype(np.int64),
-            qcode=qz["q_codes"][b, h].astype(np.float64),
+            qcode=code_values(qz["q_codes"][b, h], fmt),
             qscale=qz["q_scale"][b, h].astype(np.float64),
-            kcode=qz["k_codes"][b, j].astype(np.float64),
+            kcode=code_values(qz["k_codes"][b, j], fmt),
             kscale=qz["k_scale"][b, j][blk].astype(np.float64),
-            vhat=qz["v_scale"][b, j][blk].astype(np.float64)[:, None] * qz["v_codes"][b, j].astype(np.float64),
+            vhat=qz["v_scale"][b, j][blk].astype(np.float64)[:, None] * code_values(qz["v_codes"][b, j], fmt),
         )
     return ops
 
@@ -327,9 +412,9 @@ def attention(Qb, Kb, Vb, W: int, bits: int, idx, qz=None, block: int = 64,
 
 
 def prefill(Qb, Kb, Vb, Hkv: int, W: int, budget_ppm: int, bits: int, block: int = 64,
-            heads=None, rows=None):
+            heads=None, rows=None, fmt: str = "int"):
     """The whole path of Algorithm 2: selection, quantization, attention."""
     idx, _ = select_vertical(Qb, Kb, Hkv, W, budget_ppm)
-    qz = quantize(Qb, Kb, Vb, idx, W, bits, block)
+    qz = quantize(Qb, Kb, Vb, idx, W, bits, block, fmt)
     O = attention(Qb, Kb, Vb, W, bits, idx, qz, block, heads=heads, rows=rows)
     return dict(idx=idx, O=O, **qz)

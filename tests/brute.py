@@ -69,6 +69,49 @@ def quant_block_exact(vals, c: int):
     return codes, float(s)
 
 
+def e4m3_value_exact(code: int) -> Fraction:
+    """OCP FP8 E4M3 code -> exact rational, decoded from its fields (NaN codes
+    raise).  Written from the format definition, independently of the oracle."""
+    code = int(code) & 0xFF
+    sign = -1 if code >> 7 else 1
+    e = (code >> 3) & 0xF
+    m = code & 0x7
+    if e == 0xF and m == 0x7:
+        raise ValueError("NaN code")
+    if e == 0:
+        return sign * Fraction(m, 8) * Fraction(1, 64)
+    return sign * (1 + Fraction(m, 8)) * Fraction(2) ** (e - 7)
+
+
+def e4m3_nearest(x: Fraction, negative: bool) -> int:
+    """Nearest finite E4M3 code to the exact value x by enumeration (ties to
+    the even code; beyond +-448 the nearest is +-448); the sign bit follows
+    ``negative`` (so a negative input that rounds to zero gives 0x80)."""
+    a = abs(x)
+    best, bd = None, None
+    for code in range(127):                       # non-negative finite codes
+        d = abs(e4m3_value_exact(code) - a)
+        if bd is None or d < bd or (d == bd and code % 2 == 0 and best % 2 == 1):
+            best, bd = code, d
+    return best | (0x80 if negative else 0)
+
+
+def quant_block_fp8_exact(vals):
+    """FP8 block quantization with exact rationals: s = fl32(amax/448),
+    code = nearest E4M3 to fl32(x/s)."""
+    fr = [Fraction(float(v)) for v in vals]
+    amax = max(abs(v) for v in fr)
+    s = round_to_f32(amax / 448)
+    if s == 0:
+        return [0] * len(fr), 0.0
+    codes = []
+    for v, raw in zip(fr, vals):
+        y = round_to_f32(v / s)
+        negative = y < 0 or (y == 0 and math.copysign(1.0, float(raw)) < 0)
+        codes.append(e4m3_nearest(y, negative))
+    return codes, float(s)
+
+
 def topk_by_rank(S, k: int):
     """Position p is chosen iff fewer than k positions beat it, where p' beats p
     when S[p'] > S[p], or S[p'] == S[p] and p' < p.  Ascending output."""
@@ -82,7 +125,7 @@ def topk_by_rank(S, k: int):
 
 
 def attention_rows(Qv, Kv, Vv, L, W, bits, block, idx_list, qcodes, qscales,
-                   kcodes, kscales, vcodes, vscales):
+                   kcodes, kscales, vcodes, vscales, fp8: bool = False):
     """Scalar-loop hybrid attention for one (batch, head).
 
     Qv, Kv, Vv: lists of float rows (original positions).  idx_list: the
@@ -94,6 +137,9 @@ def attention_rows(Qv, Kv, Vv, L, W, bits, block, idx_list, qcodes, qscales,
     alpha = 1.0 / math.sqrt(D)
     P = max(0, L - W)
     vl = set(idx_list)
+
+    def cv(code):
+        return float(e4m3_value_exact(code)) if fp8 else int(code)
     qpos = [p for p in range(P) if p not in vl]          # quantized keys, ascending
     where = {p: n for n, p in enumerate(qpos)}
     out, weights = [], []
@@ -102,9 +148,9 @@ def attention_rows(Qv, Kv, Vv, L, W, bits, block, idx_list, qcodes, qscales,
         for p in range(t + 1):
             if bits != 16 and p in where:
                 n = where[p]
-                dot = sum(int(qcodes[t][d]) * int(kcodes[n][d]) for d in range(D))
+                dot = math.fsum(cv(qcodes[t][d]) * cv(kcodes[n][d]) for d in range(D))
                 z = alpha * qscales[t // block] * kscales[n] * dot
-                val = [vscales[n] * int(vcodes[n][d]) for d in range(D)]
+                val = [vscales[n] * cv(vcodes[n][d]) for d in range(D)]
             else:
                 z = alpha * math.fsum(Qv[t][d] * Kv[p][d] for d in range(D))
                 val = list(Vv[p])
