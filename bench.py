@@ -16,6 +16,7 @@ sample of the same layer.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import math
@@ -118,6 +119,10 @@ def main():
                          "is one GPU's share of config 3 under 8-way head sharding")
     ap.add_argument("--no-bits16", action="store_true",
                     help="skip the full-precision (bits 16) attention of the same inputs")
+    ap.add_argument("--fmt", choices=("int", "fp8"), default="int",
+                    help="code format of the quantized path (fp8 = OCP E4M3, 8-bit only)")
+    ap.add_argument("--no-fp8", action="store_true",
+                    help="skip the FP8-code run of the same inputs")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for rocprofv3 --pmc runs: one step, a plain 1 GiB copy kernel of known "
                          "traffic (the counter scale), one more step; no timing")
@@ -160,8 +165,9 @@ def main():
         cfg["Hq"], cfg["Hkv"] = args.hq, hkv
     Q, K, V = t(np.ascontiguousarray(d["Q"])), t(np.ascontiguousarray(d["K"])), \
         t(np.ascontiguousarray(d["V"]))
+    fmt = hyq.FMT_FP8 if args.fmt == "fp8" else hyq.FMT_INT
     shape = hyq.Shape(B=cfg["B"], Hq=cfg["Hq"], Hkv=cfg["Hkv"], L=cfg["L"], window=cfg["W"],
-                      budget_ppm=cfg["budget_ppm"], bits_kv=cfg["bits"])
+                      budget_ppm=cfg["budget_ppm"], bits_kv=cfg["bits"], kv_format=fmt)
     out_dtype = 1 if args.out_bf16 else 0
     bufs = hyq.alloc_buffers(shape, dev, out_dtype)
     z = bufs["sizes"]
@@ -246,6 +252,39 @@ def main():
                   "speedup_of_hybrid": round(ms16 / float(np.median(att)), 3)}
         del b16
 
+    # the same inputs with FP8 (E4M3) codes: quantize + attention
+    fp8 = None
+    if not args.no_fp8 and shape.bits_kv == 8 and fmt == hyq.FMT_INT:
+        s8 = dataclasses.replace(shape, kv_format=hyq.FMT_FP8)
+        b8 = hyq.alloc_buffers(s8, dev, out_dtype)
+        print("[bench] fp8 codes", file=sys.stderr, flush=True)
+        hyq.hyq_select_vertical(s8, Q, K, b8["idx"], None, b8["ws"], stream)
+
+        def step8(e=None):
+            hyq.hyq_quantize(s8, Q, K, V, b8["idx"], b8["q_codes"], b8["q_scale"],
+                             b8["k_codes"], b8["k_scale"], b8["v_codes"], b8["v_scale"],
+                             b8["kq_pos"], stream)
+            if e:
+                e[0].record(stream)
+            hyq.hyq_attn_prefill(s8, Q, K, V, b8["idx"], b8["q_codes"], b8["q_scale"],
+                                 b8["k_codes"], b8["k_scale"], b8["v_codes"], b8["v_scale"],
+                                 b8["kq_pos"], scale, b8["out"], out_dtype, stream)
+            if e:
+                e[1].record(stream)
+        for _ in range(2):
+            step8()
+        torch.cuda.synchronize()
+        e8 = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(10)]
+        for e in e8:
+            step8(e)
+        torch.cuda.synchronize()
+        ms8 = float(np.median([e[0].elapsed_time(e[1]) for e in e8]))
+        tf8 = causal_flops(shape.B, shape.Hq, shape.L, shape.D) / (ms8 * 1e-3) / 1e12
+        fp8 = {"attention_ms_median": round(ms8, 4), "tflops": round(tf8, 2),
+               "frac_fp8_peak": round(tf8 / INT8_PEAK_TOPS, 4)}
+        del b8
+
     flops = causal_flops(shape.B, shape.Hq, shape.L, shape.D)
     value = flops / (ms_step * 1e-3) / 1e12
     attn_tflops = flops / (attn_ms * 1e-3) / 1e12
@@ -259,7 +298,7 @@ def main():
                    z["q_codes_bytes"] + z["k_codes_bytes"] + z["v_codes_bytes"] +
                    z["q_scale_bytes"] + 2 * z["kv_scale_bytes"] + z["kq_pos_bytes"] + z["idx_bytes"])
     workload = (f"gqa{shape.Hq}q{shape.Hkv}kv_d{shape.D}_B{shape.B}_L{shape.L}_W{shape.window}"
-                f"_r{shape.budget_ppm}ppm_kv{shape.bits_kv}bit")
+                f"_r{shape.budget_ppm}ppm_kv{shape.bits_kv}bit" + ("_fp8" if fmt == hyq.FMT_FP8 else ""))
     traffic = load_traffic(workload)
     planted = d["planted"]
     idx = bufs["idx"].cpu().numpy()
@@ -280,7 +319,8 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "i8+f16" if shape.bits_kv != 16 else "bf16",
+        "dtype": ("bf16" if shape.bits_kv == 16 else
+                  "e4m3+f16" if fmt == hyq.FMT_FP8 else "i8+f16"),
         "data": "synthetic (seeded Gaussian Q/K/V, planted vertical lines, x10 outlier K channels)",
         "config": {"workload": workload, "B": shape.B, "Hq": shape.Hq, "Hkv": shape.Hkv,
                    "L": shape.L, "D": shape.D, "window": shape.window,
@@ -296,6 +336,7 @@ def main():
                       "select": round(float(np.median(sel)), 4),
                       "quantize": round(float(np.median(qnt)), 4)},
         "bits16_same_inputs": bits16,
+        "fp8_same_inputs": fp8,
         "attention_tflops": round(attn_tflops, 2),
         "frac_int8_peak": round(attn_tflops / INT8_PEAK_TOPS, 4),
         "frac_blended_ceiling": round(attn_tflops / BLENDED_PEAK, 4),

@@ -55,12 +55,20 @@ extern "C" {
 
 #define HYQ_KQ_POS_PAD 0x7fffffff   /* kq_pos value of padding slots */
 
+/* Code formats of the quantized path (Algorithm 2 takes B in {INT8, FP8}). */
+#define HYQ_FMT_INT 0   /* symmetric integer codes: int8 (c = 127) or int4 (c = 7) */
+#define HYQ_FMT_FP8 1   /* OCP FP8 E4M3 codes (c = 448) for Q, K and V; needs
+                           bits_kv = 8.  Each code byte is the E4M3 bit pattern of
+                           the value nearest to x / s (ties to even, saturating at
+                           +-448, zero keeps the sign of x), s = max|x| / 448.     */
+
 typedef struct hyq_shape {
   int32_t B, Hq, Hkv, L, D;  /* batch, query heads, KV heads, sequence, head dim      */
   int32_t window;            /* W >= 0: full-precision window = last W keys          */
   int32_t budget_ppm;        /* vertical ratio r in parts per million, 0..1000000    */
   int32_t bits_kv;           /* 16 (no quantization), 8 (int8) or 4 (packed int4)   */
   int32_t block;             /* quantization block in tokens (64)                   */
+  int32_t kv_format;         /* HYQ_FMT_INT or HYQ_FMT_FP8 (ignored when bits = 16) */
 } hyq_shape;
 
 typedef struct hyq_sizes {
@@ -72,7 +80,7 @@ typedef struct hyq_sizes {
   int32_t kv_row_bytes;    /* bytes per K code row: D (8-bit), D/2 (4-bit), 0 (16)   */
   size_t idx_bytes;        /* int32 idx[B][Hkv][k]                                   */
   size_t kq_pos_bytes;     /* int32 kq_pos[B][Hkv][n_kvblk*block]                    */
-  size_t q_codes_bytes;    /* int8  q_codes[B][Hq][L][D]                             */
+  size_t q_codes_bytes;    /* q_codes[B][Hq][L][D], one byte per code (int8 or E4M3) */
   size_t q_scale_bytes;    /* float q_scale[B][Hq][n_qblk]                           */
   size_t k_codes_bytes;    /* k_codes[B][Hkv][n_kvblk*block][kv_row_bytes]           */
   size_t v_codes_bytes;    /* v_codes[B][Hkv][n_kvblk][D][block*bits/8]              */

@@ -21,6 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libhyq.so")
 
 HYQ_OK, HYQ_EINVAL, HYQ_EUNSUPPORTED, HYQ_EHIP = 0, -1, -2, -3
 KQ_POS_PAD = 0x7FFFFFFF
+FMT_INT, FMT_FP8 = 0, 1       # hyq_shape.kv_format
 EXPORTED = ("hyq_sizes_for", "hyq_select_vertical", "hyq_quantize", "hyq_attn_prefill",
             "hyq_strerror", "hyq_last_error")
 
@@ -33,7 +34,8 @@ class HyqError(RuntimeError):
 
 class _Shape(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
-                ("B", "Hq", "Hkv", "L", "D", "window", "budget_ppm", "bits_kv", "block")]
+                ("B", "Hq", "Hkv", "L", "D", "window", "budget_ppm", "bits_kv", "block",
+                 "kv_format")]
 
 
 class _Sizes(ctypes.Structure):
@@ -55,6 +57,7 @@ class Shape:
     budget_ppm: int = 0
     bits_kv: int = 8
     block: int = 64
+    kv_format: int = 0      # FMT_INT or FMT_FP8
 
     def c(self) -> _Shape:
         return _Shape(*[int(getattr(self, f.name)) for f in dataclasses.fields(self)])

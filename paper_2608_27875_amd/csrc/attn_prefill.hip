@@ -7,8 +7,9 @@
 // per query row and scans
 //   segment A: the quantized keys (compacted K_Q order) in tiles of 64 =
 //              one quantization block: S^T = K_codes * Qcodes^T with the int8
-//              MFMA (exact int32), logits scaled by alpha*log2(e)*sQ*sK;
-//              P V with the f16 MFMA on the V codes (exact in f16);
+//              MFMA (exact int32) or, for FP8 codes, the E4M3 MFMA (float32),
+//              logits scaled by alpha*log2(e)*sQ*sK; P V with the f16 MFMA
+//              on the V codes (int8 and E4M3 values are exact in f16);
 //   segments B and C: the full-precision keys (vertical lines, then the
 //              window), 64 at a time gathered into LDS: S^T with the bf16
 //              MFMA; P V with the bf16 MFMA on bf16 V, P split into a high
@@ -30,18 +31,24 @@
 // softmax of tile c (one MFMA per weight pair) so that the matrix cores and
 // the vector ALUs overlap within each wave.
 //
-// V scales are folded into the exponent: P' = 2^(y - m + log2(sV/sVref))
-// with sVref a power of two >= every sV of the head, so P' <= 1 fits f16 and
-// the accumulator holds O * l / sVref.  The row sum l adds P' * (sVref/sV)
-// per tile (from the same f16 values that enter the MFMA).  Tiles whose
-// sV/sVref is below 2^-14 (including all-zero V blocks) take a slow path
-// that sums the unscaled weights instead.
+// V scales: with sVref a power of two >= every sV of the head, the ratio
+// sV/sVref = fm * 2^e is split into its mantissa fm in [1/2, 1) and its
+// power of two.  2^e is applied exactly to the V codes when they are
+// staged as f16 (a block with a small scale only ever gives small V values,
+// whose rounding stays small against the output); fm is folded into the
+// exponent, P' = 2^(y - m + log2 fm), so the f16 weights never lose range.
+// The accumulator holds O * l / sVref; the row sum l adds P' / fm per tile
+// (from the same f16 values that enter the MFMA).  An all-zero V block
+// (sV = 0) folds nothing.
 #include "hyq_internal.h"
+
+#include <type_traits>
 
 namespace hyq {
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v8i __attribute__((ext_vector_type(8)));
 typedef unsigned v4u __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef float v16f __attribute__((ext_vector_type(16)));
@@ -126,17 +133,49 @@ __device__ int count_le(const int32_t* __restrict__ a, int n, int x) {
   return lo;
 }
 
-// int8 codes (4 per dword) -> f16 pairs, exact: bytes biased to unsigned,
-// placed as the low mantissa byte of 1024 (f16 0x64xx), minus 1152.
-__device__ __forceinline__ void i8x4_to_h(uint32_t w, uint32_t& h01, uint32_t& h23) {
+// Power-of-two factor applied to the V codes of one tile while they are
+// converted to f16 (vmul = 2^e; nbias = -1152 * 2^e for the int8 route).
+struct VScale {
+  v2h vmul, nbias;
+  float f32;
+};
+
+__device__ __forceinline__ VScale make_vscale(float p2) {
+  VScale v;
+  v.vmul = v2h{(_Float16)p2, (_Float16)p2};
+  v.nbias = v2h{(_Float16)(-1152.0f * p2), (_Float16)(-1152.0f * p2)};
+  v.f32 = p2;
+  return v;
+}
+
+// int8 codes (4 per dword) -> f16 pairs of code * 2^e, exact: bytes biased to
+// unsigned, placed as the low mantissa byte of 1024 (f16 0x64xx), then one
+// fused (x * 2^e - 1152 * 2^e) per pair.
+__device__ __forceinline__ void i8x4_to_h(uint32_t w, uint32_t& h01, uint32_t& h23,
+                                          const VScale& vs) {
   const uint32_t u = w ^ 0x80808080u;
   const uint32_t a = __builtin_amdgcn_perm(0x64646464u, u, 0x04010400u);
   const uint32_t b = __builtin_amdgcn_perm(0x64646464u, u, 0x04030402u);
-  const v2h bias = {(_Float16)1152.0f, (_Float16)1152.0f};
-  const v2h ha = __builtin_bit_cast(v2h, a) - bias;
-  const v2h hb = __builtin_bit_cast(v2h, b) - bias;
+  const v2h ha = __builtin_elementwise_fma(__builtin_bit_cast(v2h, a), vs.vmul, vs.nbias);
+  const v2h hb = __builtin_elementwise_fma(__builtin_bit_cast(v2h, b), vs.vmul, vs.nbias);
   h01 = __builtin_bit_cast(uint32_t, ha);
   h23 = __builtin_bit_cast(uint32_t, hb);
+}
+
+// Four E4M3 codes (one per byte) -> f16 pairs of value * 2^e, exact unless
+// the result is below the f16 range (the conversion applies power-of-two
+// scales exactly).
+__device__ __forceinline__ void e4m3x4_to_h(uint32_t w, uint32_t& h01, uint32_t& h23,
+                                            const VScale& vs) {
+  h01 = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, vs.f32, false));
+  h23 = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, vs.f32, true));
+}
+
+template <int FMT>
+__device__ __forceinline__ void codes4_to_h(uint32_t w, uint32_t& h01, uint32_t& h23,
+                                            const VScale& vs) {
+  if constexpr (FMT == HYQ_FMT_FP8) e4m3x4_to_h(w, h01, h23, vs);
+  else i8x4_to_h(w, h01, h23, vs);
 }
 
 // Packed int4 (8 nibbles, element 2i low / 2i+1 high in byte i) -> 8 int8 of
@@ -171,17 +210,82 @@ struct StageRegs {
   int32_t meta;                 // threads 0..63: kq_pos; 64, 65: sK, sV bits (K's tile)
 };
 
-// K fragments of one tile for the S^T product (A operands, 2 halves x 4 steps).
+// K fragments of one tile for the S^T product (A operands of the two 32-key
+// halves).  int8: 4 steps of v_mfma_i32_32x32x32_i8, lane half h holding
+// channels 32*step + 16h .. +16; E4M3: 2 steps of
+// v_mfma_scale_f32_32x32x64_f8f6f4, lane half h holding channels
+// 64*step + 32h .. +32.  Q fragments (the B operands) split the channels the
+// same way, which is all the dot product needs.
+template <int FMT>
 struct KFrag {
   v4i f[2][4];
 };
+template <>
+struct KFrag<HYQ_FMT_FP8> {
+  v8i f[2][2];
+};
+template <int FMT>
+struct QFrag {
+  v4i f[4];
+};
+template <>
+struct QFrag<HYQ_FMT_FP8> {
+  v8i f[2];
+};
 
-__device__ __forceinline__ void read_kfrag(KFrag& kf, const KBuf& b, int col, int half) {
+template <int FMT>
+__device__ __forceinline__ void read_kfrag(KFrag<FMT>& kf, const KBuf& b, int col, int half) {
 #pragma unroll
-  for (int kh = 0; kh < 2; ++kh)
+  for (int kh = 0; kh < 2; ++kh) {
+    if constexpr (FMT == HYQ_FMT_FP8) {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const v4i lo = *reinterpret_cast<const v4i*>(b.k + kswz(kh * 32 + col, kk * 4 + half * 2));
+        const v4i hi = *reinterpret_cast<const v4i*>(b.k + kswz(kh * 32 + col, kk * 4 + half * 2 + 1));
+        kf.f[kh][kk] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+    } else {
+#pragma unroll
+      for (int k4 = 0; k4 < 4; ++k4)
+        kf.f[kh][k4] = *reinterpret_cast<const v4i*>(b.k + kswz(kh * 32 + col, k4 * 2 + half));
+    }
+  }
+}
+
+template <int FMT>
+__device__ __forceinline__ void read_qfrag(QFrag<FMT>& qf, const int8_t* qrow, bool ok, int half) {
+  if constexpr (FMT == HYQ_FMT_FP8) {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+      qf.f[kk] = ok ? *reinterpret_cast<const v8i*>(qrow + kk * 64 + half * 32) : v8i{};
+  } else {
 #pragma unroll
     for (int k4 = 0; k4 < 4; ++k4)
-      kf.f[kh][k4] = *reinterpret_cast<const v4i*>(b.k + kswz(kh * 32 + col, k4 * 2 + half));
+      qf.f[k4] = ok ? *reinterpret_cast<const v4i*>(qrow + k4 * 32 + half * 16) : v4i{};
+  }
+}
+
+// S^T of one tile: int32 (int8 codes) or float32 (E4M3 codes) logits.
+template <int FMT>
+using SVec = std::conditional_t<FMT == HYQ_FMT_FP8, v16f, v16i>;
+
+template <int FMT>
+__device__ __forceinline__ void qk_tile(SVec<FMT> (&s)[2], const KFrag<FMT>& kf,
+                                        const QFrag<FMT>& qf) {
+#pragma unroll
+  for (int kh = 0; kh < 2; ++kh) {
+    s[kh] = SVec<FMT>{};
+    if constexpr (FMT == HYQ_FMT_FP8) {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)   // format 0 = E4M3 for both operands, unit scales
+        s[kh] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kf.f[kh][kk], qf.f[kk], s[kh], 0,
+                                                                0, 0, 127, 0, 127);
+    } else {
+#pragma unroll
+      for (int k4 = 0; k4 < 4; ++k4)
+        s[kh] = __builtin_amdgcn_mfma_i32_32x32x32_i8(kf.f[kh][k4], qf.f[k4], s[kh], 0, 0, 0);
+    }
+  }
 }
 
 // Everything one wave needs for the quantized segment.
@@ -225,8 +329,9 @@ __device__ __forceinline__ void stage_load(StageRegs<BITS>& r, const SegA& a, in
 // int8 K: chunk q = row*8 + j goes to the swizzled slot of (row, j).  4-bit
 // K: chunk tid holds 32 channels of row tid/4, expanded to int8 (16*code)
 // and stored as two chunks.  V: f16 [128][kVPitch] in the permuted key order.
-template <int BITS>
-__device__ __forceinline__ void stage_store(KBuf& kb, VBuf& vb, const StageRegs<BITS>& r, int tid) {
+template <int BITS, int FMT>
+__device__ __forceinline__ void stage_store(KBuf& kb, VBuf& vb, const StageRegs<BITS>& r, int tid,
+                                            const VScale& vs) {
   if (BITS == 8) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -239,10 +344,10 @@ __device__ __forceinline__ void stage_store(KBuf& kb, VBuf& vb, const StageRegs<
       const int d = q >> 2, kg = q & 3;   // channel d, keys kg*16 .. +16
       const v4u w = r.v[i];
       uint32_t h[8];
-      i8x4_to_h(w.x, h[0], h[1]);   // keys 0..3
-      i8x4_to_h(w.y, h[2], h[3]);   // keys 4..7
-      i8x4_to_h(w.z, h[4], h[5]);   // keys 8..11
-      i8x4_to_h(w.w, h[6], h[7]);   // keys 12..15
+      codes4_to_h<FMT>(w.x, h[0], h[1], vs);   // keys 0..3
+      codes4_to_h<FMT>(w.y, h[2], h[3], vs);   // keys 4..7
+      codes4_to_h<FMT>(w.z, h[4], h[5], vs);   // keys 8..11
+      codes4_to_h<FMT>(w.w, h[6], h[7], vs);   // keys 12..15
       uint8_t* dst = vb.v + d * kVPitch + kg * 32;
       *reinterpret_cast<v4u*>(dst) = v4u{h[0], h[1], h[4], h[5]};
       *reinterpret_cast<v4u*>(dst + 16) = v4u{h[2], h[3], h[6], h[7]};
@@ -268,10 +373,10 @@ __device__ __forceinline__ void stage_store(KBuf& kb, VBuf& vb, const StageRegs<
       i4x8_to_i8(ww[2 * g16], bb[0], bb[1]);
       i4x8_to_i8(ww[2 * g16 + 1], bb[2], bb[3]);
       uint32_t h[8];
-      i8x4_to_h(bb[0], h[0], h[1]);
-      i8x4_to_h(bb[1], h[2], h[3]);
-      i8x4_to_h(bb[2], h[4], h[5]);
-      i8x4_to_h(bb[3], h[6], h[7]);
+      i8x4_to_h(bb[0], h[0], h[1], vs);
+      i8x4_to_h(bb[1], h[2], h[3], vs);
+      i8x4_to_h(bb[2], h[4], h[5], vs);
+      i8x4_to_h(bb[3], h[6], h[7], vs);
       uint8_t* dst = vb.v + d * kVPitch + (kh * 2 + g16) * 32;
       *reinterpret_cast<v4u*>(dst) = v4u{h[0], h[1], h[4], h[5]};
       *reinterpret_cast<v4u*>(dst + 16) = v4u{h[2], h[3], h[6], h[7]};
@@ -325,11 +430,6 @@ struct NState {
   v16f acc[4];    // O^T accumulator, 4 groups of 32 channels
 };
 
-__device__ __forceinline__ int xhalf_max_i(int x) {
-  const auto r = __builtin_amdgcn_permlane32_swap((unsigned)x, (unsigned)x, false, false);
-  return max((int)r[0], (int)r[1]);
-}
-
 // Key index (0..63) of accumulator register r of half-tile kh for this lane.
 __device__ __forceinline__ int key_of(int kh, int r, int half) {
   return kh * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
@@ -358,29 +458,28 @@ __device__ __forceinline__ void apply_corr(NState& ns) {
   ns.corr = 1.0f;
 }
 
-// General path: causal mask by original position, tiny V scales, or a tile
-// whose maximum outgrew the reference max.  Raises m to the masked tile
+// General path: causal mask by original position, or a tile whose maximum
+// outgrew the reference max.  Raises m to the masked tile
 // maximum when needed and rescales l and the accumulator at once (the
 // accumulator already holds every P V product of earlier tiles).  No
 // per-lane branches, so the cross-lane swap sees every lane's operand; the
 // visibility test is evaluated twice rather than kept in registers.
-__device__ __forceinline__ void softmax_general(NState& ns, const v16i (&s)[2], v8h (&p)[4],
-                                             float cqk, float f, bool diag, const int32_t* pos,
+template <typename SV>
+__device__ __forceinline__ void softmax_general(NState& ns, const SV (&s)[2], v8h (&p)[4],
+                                             float cqk, float fm, bool diag, const int32_t* pos,
                                              int tq, int half) {
-  int mi = INT_MIN;
+  float mx = -INFINITY;
 #pragma unroll
   for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const bool vis = (!diag) | (pos[key_of(kh, r, half)] <= tq);
-      mi = max(mi, vis ? s[kh][r] : INT_MIN);
+      mx = fmaxf(mx, vis ? (float)s[kh][r] : -INFINITY);
     }
-  mi = xhalf_max_i(mi);
-  lazy_max(ns, mi == INT_MIN ? -INFINITY : (float)mi * cqk);
+  mx = xhalf_max(mx);
+  lazy_max(ns, mx == -INFINITY ? -INFINITY : mx * cqk);
   apply_corr(ns);
-  // The row sum adds the same f16 weights the MFMA uses (divided by f),
-  // unless f is so small that they lose precision; then the float32 ones.
-  const bool f_ok = f >= 6.103515625e-05f;
+  // the row sum adds the same f16 weights the MFMA uses, divided by fm
   float ps = 0.0f;
 #pragma unroll
   for (int kh = 0; kh < 2; ++kh)
@@ -388,12 +487,11 @@ __device__ __forceinline__ void softmax_general(NState& ns, const v16i (&s)[2], 
     for (int r = 0; r < 16; ++r) {
       const bool vis = (!diag) | (pos[key_of(kh, r, half)] <= tq);
       const float ex = __builtin_amdgcn_exp2f((float)s[kh][r] * cqk - ns.m);
-      const float e = vis ? ex : 0.0f;
-      const _Float16 hp = (_Float16)(e * f);
-      ps += f_ok ? (float)hp : e;
+      const _Float16 hp = (_Float16)((vis ? ex : 0.0f) * fm);
+      ps += (float)hp;
       p[kh * 2 + (r >> 3)][r & 7] = hp;
     }
-  ns.l += f_ok ? ps * __builtin_amdgcn_rcpf(f) : ps;
+  ns.l += ps * __builtin_amdgcn_rcpf(fm);
 }
 
 // One tile of the quantized segment:
@@ -407,10 +505,10 @@ __device__ __forceinline__ void softmax_general(NState& ns, const v16i (&s)[2], 
 // general path moves the reference max, and it rescales on the spot.
 // PH = c % 4 is a template argument so that every LDS address is a per-lane
 // constant plus an immediate offset.
-template <int BITS, int PH>
-__device__ __forceinline__ void segA_tile(Smem& sm, const SegA& a, int c, const v4i (&qf)[4],
+template <int BITS, int FMT, int PH>
+__device__ __forceinline__ void segA_tile(Smem& sm, const SegA& a, int c, const QFrag<FMT>& qf,
                                           NState& st, const v8h (&pprev)[4], v8h (&pcur)[4],
-                                          StageRegs<BITS>& sr, KFrag& kf) {
+                                          StageRegs<BITS>& sr, KFrag<FMT>& kf) {
   constexpr float kSub = BITS == 8 ? 1.0f : 0.0625f;   // 4-bit codes are staged as 16*code
   const int tid = threadIdx.x;
   const KBuf& cur = sm.q.kb[PH];
@@ -418,20 +516,22 @@ __device__ __forceinline__ void segA_tile(Smem& sm, const SegA& a, int c, const 
   const float sk = __int_as_float(cur.pos[kMetaSK]) * kSub;
   const float sv = __int_as_float(cur.pos[kMetaSV]) * kSub;
   const int last = __builtin_amdgcn_readfirstlane(cur.pos[kTile - 1]);
+  // sV / sVref = fm * 2^ev (sVref a power of two: the product is exact)
+  int ev;
+  float fm = __builtin_frexpf(sv * a.inv_vref, &ev);
+  if (!(sv > 0.0f)) {   // all-zero V block: its V codes are 0, fold nothing
+    fm = 1.0f;
+    ev = 0;
+  }
+  const VScale vs = make_vscale(__builtin_ldexpf(1.0f, ev));
 
   // S^T of tile c (its K fragments arrived during the previous tile)
-  v16i s[2];
-#pragma unroll
-  for (int kh = 0; kh < 2; ++kh) {
-    s[kh] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-    for (int k4 = 0; k4 < 4; ++k4)
-      s[kh] = __builtin_amdgcn_mfma_i32_32x32x32_i8(kf.f[kh][k4], qf[k4], s[kh], 0, 0, 0);
-  }
+  SVec<FMT> s[2];
+  qk_tile<FMT>(s, kf, qf);
   // publish K(c+2) and V(c) (registers loaded during tile c-1) and load K(c+3)
   // and V(c+1); the conversion runs in the shadow of the MFMAs above.  Past
   // the end the last tile is staged again into the free buffers (no branch).
-  stage_store<BITS>(sm.q.kb[(PH + 2) % kKRing], sm.q.vb[PH & 1], sr, tid);
+  stage_store<BITS, FMT>(sm.q.kb[(PH + 2) % kKRing], sm.q.vb[PH & 1], sr, tid, vs);
   stage_load<BITS>(sr, a, min(c + 3, a.n - 1), min(c + 1, a.n - 1), tid);
 
   // Fast path: weights against the current reference max, without the tile
@@ -439,8 +539,7 @@ __device__ __forceinline__ void segA_tile(Smem& sm, const SegA& a, int c, const 
   // weight may have left the f16 range).  Step i issues the MFMA of
   // (channel group i%4, key group i/4) of P V(c-1) and the weight pair i.
   const float cqk = a.cq * sk;
-  const float f = sv * a.inv_vref;
-  const float bias = __builtin_amdgcn_logf(f) - st.m;   // log2
+  const float bias = __builtin_amdgcn_logf(fm) - st.m;   // log2
   const v2h one2 = {(_Float16)1.0f, (_Float16)1.0f};
   float ps = 0.0f;
 #pragma unroll
@@ -463,19 +562,19 @@ __device__ __forceinline__ void segA_tile(Smem& sm, const SegA& a, int c, const 
   // than sunk into the branch below that consumes them
   asm volatile("" : "+v"(pcur[0]), "+v"(pcur[1]), "+v"(pcur[2]), "+v"(pcur[3]), "+v"(ps));
   const bool diag = last > a.t0;
-  const bool redo = diag || !(f >= 6.103515625e-05f) || __ballot(!(ps <= kFastMax)) != 0;
+  const bool redo = diag || __ballot(!(ps <= kFastMax)) != 0;
   if (redo) {
-    softmax_general(st, s, pcur, cqk, f, diag, cur.pos, a.t0 + a.col, a.half);
+    softmax_general(st, s, pcur, cqk, fm, diag, cur.pos, a.t0 + a.col, a.half);
   } else {
-    st.l = __builtin_fmaf(ps, __builtin_amdgcn_rcpf(f), st.l);   // 1-ulp reciprocal
+    st.l = __builtin_fmaf(ps, __builtin_amdgcn_rcpf(fm), st.l);   // 1-ulp reciprocal
   }
   // K fragments of tile c+1 (published by the previous barrier); past the
   // end they read a staged copy and are not used
-  read_kfrag(kf, sm.q.kb[(PH + 1) % kKRing], a.col, a.half);
+  read_kfrag<FMT>(kf, sm.q.kb[(PH + 1) % kKRing], a.col, a.half);
   __syncthreads();
 }
 
-template <int BITS, int OUT_BF16>
+template <int BITS, int OUT_BF16, int FMT>
 __global__ void __launch_bounds__(kThreads, 2)
 attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                     const uint16_t* __restrict__ V, const int32_t* __restrict__ idx,
@@ -572,28 +671,24 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
     a.half = half;
     a.col = col;
 
-    v4i qf[4];
-    {
-      const int8_t* qrow = q_codes + (bh * L + (row_ok ? tq : 0)) * kHeadDim;
-#pragma unroll
-      for (int k4 = 0; k4 < 4; ++k4)
-        qf[k4] = row_ok ? *reinterpret_cast<const v4i*>(qrow + k4 * 32 + half * 16) : v4i{0, 0, 0, 0};
-    }
+    QFrag<FMT> qf;
+    read_qfrag<FMT>(qf, q_codes + (bh * L + (row_ok ? tq : 0)) * kHeadDim, row_ok, half);
 
     // prologue: K(0), K(1) into LDS, K(2) and V(0) into registers, the
     // fragments of K(0) read; the V buffer that tile 0 multiplies by zero
     // weights is cleared (no stale NaNs)
     StageRegs<BITS> sr;
     stage_load<BITS>(sr, a, 0, 0, threadIdx.x);
-    stage_store<BITS>(sm.q.kb[0], sm.q.vb[1], sr, threadIdx.x);
+    const VScale unit = make_vscale(1.0f);   // the V written here is cleared below
+    stage_store<BITS, FMT>(sm.q.kb[0], sm.q.vb[1], sr, threadIdx.x, unit);
     stage_load<BITS>(sr, a, min(1, nq_tiles - 1), 0, threadIdx.x);
-    stage_store<BITS>(sm.q.kb[1], sm.q.vb[1], sr, threadIdx.x);
+    stage_store<BITS, FMT>(sm.q.kb[1], sm.q.vb[1], sr, threadIdx.x, unit);
     stage_load<BITS>(sr, a, min(2, nq_tiles - 1), 0, threadIdx.x);
     __syncthreads();
     for (int i = threadIdx.x; i < kVBytes / 16; i += kThreads)
       reinterpret_cast<v4u*>(sm.q.vb[1].v)[i] = v4u{0u, 0u, 0u, 0u};
-    KFrag kf;
-    read_kfrag(kf, sm.q.kb[0], col, half);
+    KFrag<FMT> kf;
+    read_kfrag<FMT>(kf, sm.q.kb[0], col, half);
     __syncthreads();
 
     // the P V of tile c runs in iteration c+1, next to the softmax of c+1;
@@ -605,14 +700,14 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
       for (int e = 0; e < 8; ++e) pa[i][e] = pb[i][e] = (_Float16)0.0f;
     int c = 0;
     for (; c + 3 < nq_tiles; c += 4) {
-      segA_tile<BITS, 0>(sm, a, c, qf, st, pa, pb, sr, kf);
-      segA_tile<BITS, 1>(sm, a, c + 1, qf, st, pb, pa, sr, kf);
-      segA_tile<BITS, 2>(sm, a, c + 2, qf, st, pa, pb, sr, kf);
-      segA_tile<BITS, 3>(sm, a, c + 3, qf, st, pb, pa, sr, kf);
+      segA_tile<BITS, FMT, 0>(sm, a, c, qf, st, pa, pb, sr, kf);
+      segA_tile<BITS, FMT, 1>(sm, a, c + 1, qf, st, pb, pa, sr, kf);
+      segA_tile<BITS, FMT, 2>(sm, a, c + 2, qf, st, pa, pb, sr, kf);
+      segA_tile<BITS, FMT, 3>(sm, a, c + 3, qf, st, pb, pa, sr, kf);
     }
-    if (c < nq_tiles) segA_tile<BITS, 0>(sm, a, c, qf, st, pa, pb, sr, kf);
-    if (c + 1 < nq_tiles) segA_tile<BITS, 1>(sm, a, c + 1, qf, st, pb, pa, sr, kf);
-    if (c + 2 < nq_tiles) segA_tile<BITS, 2>(sm, a, c + 2, qf, st, pa, pb, sr, kf);
+    if (c < nq_tiles) segA_tile<BITS, FMT, 0>(sm, a, c, qf, st, pa, pb, sr, kf);
+    if (c + 1 < nq_tiles) segA_tile<BITS, FMT, 1>(sm, a, c + 1, qf, st, pb, pa, sr, kf);
+    if (c + 2 < nq_tiles) segA_tile<BITS, FMT, 2>(sm, a, c + 2, qf, st, pa, pb, sr, kf);
     // P V of the last tile
     const v8h (&plast)[4] = (nq_tiles & 1) ? pb : pa;
     const VBuf& lb = sm.q.vb[(nq_tiles - 1) & 1];
@@ -723,7 +818,7 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
     }
 }
 
-template <int BITS, int OB>
+template <int BITS, int OB, int FMT>
 hipError_t launch_t(const hyq_shape& s, const hyq_sizes& z, const uint16_t* Q,
                     const uint16_t* K, const uint16_t* V, const int32_t* idx,
                     const int8_t* q_codes, const float* q_scale, const uint8_t* k_codes,
@@ -734,7 +829,7 @@ hipError_t launch_t(const hyq_shape& s, const hyq_sizes& z, const uint16_t* Q,
   const int wg_per_bj = (g * nrb + kWaves - 1) / kWaves;
   const int nbj = s.B * s.Hkv;
   const dim3 grid(wg_per_bj * nbj);
-  attn_prefill_kernel<BITS, OB><<<grid, kThreads, 0, st>>>(
+  attn_prefill_kernel<BITS, OB, FMT><<<grid, kThreads, 0, st>>>(
       Q, K, V, idx, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, kq_pos, out, s.Hq,
       s.Hkv, nbj, s.L, z.P, z.k, z.nQ, z.n_qblk, z.n_kvblk, softmax_scale * kLog2e);
   return hipGetLastError();
@@ -749,18 +844,21 @@ hipError_t launch_attn_prefill(const hyq_shape& s, const hyq_sizes& z, const uin
                                const uint8_t* v_codes, const float* v_scale,
                                const int32_t* kq_pos, float softmax_scale, void* out,
                                int out_dtype, hipStream_t st) {
-#define HYQ_LAUNCH(BITS, OB)                                                                  \
-  return launch_t<BITS, OB>(s, z, Q, K, V, idx, q_codes, q_scale, k_codes, k_scale, v_codes, \
-                            v_scale, kq_pos, softmax_scale, out, st)
+#define HYQ_LAUNCH(BITS, OB, FMT)                                                              \
+  return launch_t<BITS, OB, FMT>(s, z, Q, K, V, idx, q_codes, q_scale, k_codes, k_scale,       \
+                                 v_codes, v_scale, kq_pos, softmax_scale, out, st)
   if (s.bits_kv == 16) {
-    if (out_dtype) HYQ_LAUNCH(16, 1);
-    HYQ_LAUNCH(16, 0);
+    if (out_dtype) HYQ_LAUNCH(16, 1, HYQ_FMT_INT);
+    HYQ_LAUNCH(16, 0, HYQ_FMT_INT);
+  } else if (s.bits_kv == 8 && s.kv_format == HYQ_FMT_FP8) {
+    if (out_dtype) HYQ_LAUNCH(8, 1, HYQ_FMT_FP8);
+    HYQ_LAUNCH(8, 0, HYQ_FMT_FP8);
   } else if (s.bits_kv == 8) {
-    if (out_dtype) HYQ_LAUNCH(8, 1);
-    HYQ_LAUNCH(8, 0);
+    if (out_dtype) HYQ_LAUNCH(8, 1, HYQ_FMT_INT);
+    HYQ_LAUNCH(8, 0, HYQ_FMT_INT);
   } else {
-    if (out_dtype) HYQ_LAUNCH(4, 1);
-    HYQ_LAUNCH(4, 0);
+    if (out_dtype) HYQ_LAUNCH(4, 1, HYQ_FMT_INT);
+    HYQ_LAUNCH(4, 0, HYQ_FMT_INT);
   }
 #undef HYQ_LAUNCH
 }

@@ -43,6 +43,10 @@ int check_shape(const hyq_shape* s, hyq_sizes* z) {
   if (s->block < 1) return fail(HYQ_EINVAL, "block must be >= 1 (got %d)", s->block);
   if (s->bits_kv != 16 && s->bits_kv != 8 && s->bits_kv != 4)
     return fail(HYQ_EUNSUPPORTED, "bits_kv must be 16, 8 or 4 (got %d)", s->bits_kv);
+  if (s->kv_format != HYQ_FMT_INT && s->kv_format != HYQ_FMT_FP8)
+    return fail(HYQ_EINVAL, "kv_format must be HYQ_FMT_INT or HYQ_FMT_FP8 (got %d)", s->kv_format);
+  if (s->kv_format == HYQ_FMT_FP8 && s->bits_kv == 4)
+    return fail(HYQ_EINVAL, "FP8 codes need bits_kv = 8 (got 4)");
   if (s->D != hyq::kHeadDim)
     return fail(HYQ_EUNSUPPORTED, "head dim %d not supported (only %d)", s->D, hyq::kHeadDim);
   if (s->block != hyq::kBlock)

@@ -7,7 +7,10 @@
 //   K, V    : blocks of 64 consecutive entries of the compacted K_Q sequence
 //             (rows gathered through kq_pos);
 //   s = fl32(max|x| / c), code = clamp(rint(fl32(x / s)), -c, c), s = 0 ->
-//   codes 0 (c = 127 for 8-bit, 7 for 4-bit).
+//   codes 0 (c = 127 for 8-bit, 7 for 4-bit);
+//   FP8 codes (c = 448): the OCP E4M3 value nearest to fl32(x / s), ties to
+//   even, saturating at +-448, zero keeping the sign (the hardware
+//   float32 -> E4M3 conversion, which rounds to nearest even).
 //
 // The division is the IEEE correctly rounded float32 division (no
 // reciprocal shortcut) and rint rounds half to even, so codes match the
@@ -84,10 +87,25 @@ __device__ __forceinline__ int quant1(float x, float s, float c) {
   return (int)fminf(fmaxf(q, -c), c);
 }
 
+// E4M3 bit pattern of x / s (s > 0); the clamp keeps -0 and bounds the
+// quotient by the largest finite value.
+__device__ __forceinline__ int quant1_fp8(float x, float s) {
+  const float y = fminf(fmaxf(x / s, -448.0f), 448.0f);
+  return __builtin_amdgcn_cvt_pk_fp8_f32(y, 0.0f, 0, false) & 0xff;
+}
+
+template <int FMT>
+__device__ __forceinline__ int quant_code(float x, float s, float c) {
+  if (FMT == HYQ_FMT_FP8) return quant1_fp8(x, s);
+  return quant1(x, s, c);
+}
+
 // Thread layout of one 64 x 128 block: row = tid / 4, channels (tid % 4) * 32 .. +32.
+template <int FMT>
 __global__ void __launch_bounds__(kQuantThreads)
 quant_q_kernel(const uint16_t* __restrict__ Q, int8_t* __restrict__ qc, float* __restrict__ qs,
                int L, int n_qblk) {
+  constexpr float C = FMT == HYQ_FMT_FP8 ? 448.0f : 127.0f;
   __shared__ float red[kQuantThreads / 64];
   const int bh = blockIdx.y, blk = blockIdx.x;
   const int row = threadIdx.x >> 2, c0 = (threadIdx.x & 3) * 32;
@@ -103,7 +121,7 @@ quant_q_kernel(const uint16_t* __restrict__ Q, int8_t* __restrict__ qc, float* _
 #pragma unroll
   for (int e = 0; e < 32; ++e) m = fmaxf(m, fabsf(x[e]));
   const float amax = block_max(m, red);
-  const float s = amax / 127.0f;
+  const float s = amax / C;
   if (threadIdx.x == 0) qs[(size_t)bh * n_qblk + blk] = s;
   if (t >= L) return;
   uint32_t packed[8];
@@ -112,7 +130,7 @@ quant_q_kernel(const uint16_t* __restrict__ Q, int8_t* __restrict__ qc, float* _
     uint32_t w = 0;
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
-      const int code = s > 0.0f ? quant1(x[4 * e + b], s, 127.0f) : 0;
+      const int code = s > 0.0f ? quant_code<FMT>(x[4 * e + b], s, C) : 0;
       w |= (uint32_t)(code & 0xff) << (8 * b);
     }
     packed[e] = w;
@@ -124,13 +142,14 @@ quant_q_kernel(const uint16_t* __restrict__ Q, int8_t* __restrict__ qc, float* _
 
 // One workgroup per (b, j, compacted block).  K codes are written row-major,
 // V codes channel-major (the block transposed) through an LDS tile.
-template <int BITS>
+template <int BITS, int FMT>
 __global__ void __launch_bounds__(kQuantThreads)
 quant_kv_kernel(const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
                 const int32_t* __restrict__ kq_pos, uint8_t* __restrict__ kc,
                 float* __restrict__ ks, uint8_t* __restrict__ vc, float* __restrict__ vs,
                 int L, int nQ, int n_kvblk) {
-  constexpr float C = BITS == 8 ? 127.0f : 7.0f;
+  static_assert(FMT == HYQ_FMT_INT || BITS == 8, "FP8 codes are 8-bit");
+  constexpr float C = FMT == HYQ_FMT_FP8 ? 448.0f : (BITS == 8 ? 127.0f : 7.0f);
   constexpr int kRow = BITS == 8 ? kHeadDim : kHeadDim / 2;   // bytes per K code row
   constexpr int vRow = BITS == 8 ? kBlock : kBlock / 2;        // bytes per V code row (one channel)
   __shared__ float red[kQuantThreads / 64];
@@ -163,8 +182,8 @@ quant_kv_kernel(const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
   int ck[32], cv[32];
 #pragma unroll
   for (int e = 0; e < 32; ++e) {
-    ck[e] = sk > 0.0f ? quant1(xk[e], sk, C) : 0;
-    cv[e] = sv > 0.0f ? quant1(xv[e], sv, C) : 0;
+    ck[e] = sk > 0.0f ? quant_code<FMT>(xk[e], sk, C) : 0;
+    cv[e] = sv > 0.0f ? quant_code<FMT>(xv[e], sv, C) : 0;
   }
   // K: row-major codes
   uint8_t* kdst = kc + ((size_t)bj * slots + n) * kRow;
@@ -235,16 +254,23 @@ hipError_t launch_quantize(const hyq_shape& s, const hyq_sizes& z, const uint16_
     dim3 cg((span + 255) / 256, BHkv);
     compact_kernel<<<cg, 256, 0, st>>>(idx, kq_pos, z.k, z.P, z.nQ, nslots);
   }
+  const bool fp8 = s.kv_format == HYQ_FMT_FP8;
   dim3 qg(z.n_qblk, s.B * s.Hq);
-  quant_q_kernel<<<qg, kQuantThreads, 0, st>>>(Q, q_codes, q_scale, s.L, z.n_qblk);
+  if (fp8)
+    quant_q_kernel<HYQ_FMT_FP8><<<qg, kQuantThreads, 0, st>>>(Q, q_codes, q_scale, s.L, z.n_qblk);
+  else
+    quant_q_kernel<HYQ_FMT_INT><<<qg, kQuantThreads, 0, st>>>(Q, q_codes, q_scale, s.L, z.n_qblk);
   if (z.n_kvblk > 0) {
     dim3 kg(z.n_kvblk, BHkv);
-    if (s.bits_kv == 8)
-      quant_kv_kernel<8><<<kg, kQuantThreads, 0, st>>>(K, V, kq_pos, k_codes, k_scale, v_codes,
-                                                       v_scale, s.L, z.nQ, z.n_kvblk);
+    if (fp8)
+      quant_kv_kernel<8, HYQ_FMT_FP8><<<kg, kQuantThreads, 0, st>>>(
+          K, V, kq_pos, k_codes, k_scale, v_codes, v_scale, s.L, z.nQ, z.n_kvblk);
+    else if (s.bits_kv == 8)
+      quant_kv_kernel<8, HYQ_FMT_INT><<<kg, kQuantThreads, 0, st>>>(
+          K, V, kq_pos, k_codes, k_scale, v_codes, v_scale, s.L, z.nQ, z.n_kvblk);
     else
-      quant_kv_kernel<4><<<kg, kQuantThreads, 0, st>>>(K, V, kq_pos, k_codes, k_scale, v_codes,
-                                                       v_scale, s.L, z.nQ, z.n_kvblk);
+      quant_kv_kernel<4, HYQ_FMT_INT><<<kg, kQuantThreads, 0, st>>>(
+          K, V, kq_pos, k_codes, k_scale, v_codes, v_scale, s.L, z.nQ, z.n_kvblk);
   }
   return hipGetLastError();
 }

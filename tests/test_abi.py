@@ -70,6 +70,8 @@ def test_sizes_match_oracle(lib, L, W, ppm, bits):
     (dict(block=0), hyq.HYQ_EINVAL),
     (dict(D=64), hyq.HYQ_EUNSUPPORTED), (dict(bits_kv=5), hyq.HYQ_EUNSUPPORTED),
     (dict(block=32), hyq.HYQ_EUNSUPPORTED), (dict(Hq=72, Hkv=8), hyq.HYQ_EUNSUPPORTED),
+    (dict(kv_format=2), hyq.HYQ_EINVAL), (dict(kv_format=-1), hyq.HYQ_EINVAL),
+    (dict(kv_format=hyq.FMT_FP8, bits_kv=4), hyq.HYQ_EINVAL),
 ])
 def test_bad_shapes_rejected(lib, kw, code):
     with pytest.raises(hyq.HyqError) as e:

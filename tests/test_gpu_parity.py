@@ -52,6 +52,35 @@ def test_small_full_parity(case):
     assert mx <= gc.TOL_MAX and mean <= gc.TOL_MEAN
 
 
+@pytest.mark.parametrize("bits", [8, 4])
+def test_v_outlier_block(bits):
+    """One huge V entry (3e4) makes its block's scale (and sVref) dwarf every
+    other block's; the other blocks must keep their precision.  Also zero
+    blocks, exact zeros and negative zeros in Q, K and V.  Outputs on the
+    outlier channel reach ~1e3, so the bound there scales with the row's
+    magnitude; the mean-abs bound holds over the other channels."""
+    L, W = 520, 40
+    d = _inputs("v_outlier", 1, 4, 1, L, W)
+    for name in ("Q", "K", "V"):
+        x = gen.bf16_bits_to_f32(d[name])
+        x[..., 3] = 0.0
+        x[..., 5] = -0.0
+        x[..., 64:128, :] = 0.0
+        if name == "V":
+            x[..., 200, 9] = 3.0e4
+        d[name] = gen.f32_to_bf16_bits(x)
+    shape = gc.hyq.Shape(B=1, Hq=4, Hkv=1, L=L, window=W, budget_ppm=30000, bits_kv=bits)
+    g = gc.run_gpu(shape, d)
+    idx, qz = gc.check_select_quant(shape, d, g)
+    O = orc.attention(d["Q"], d["K"], d["V"], W, bits, idx, qz)
+    Og = g["out"].reshape(O.shape)
+    rel = gc.scaled_error(Og, O)
+    keep = np.arange(O.shape[-1]) != 9
+    mx, mean = gc.attention_error(Og[..., keep], O[..., keep])
+    print(f"  scaled max {rel:.3e}; other channels max-abs {mx:.3e} mean-abs {mean:.3e}", flush=True)
+    assert rel <= gc.TOL_MAX and mx <= gc.TOL_MAX and mean <= gc.TOL_MEAN
+
+
 def test_deterministic_and_bf16_output():
     d = _inputs("det", 1, 8, 2, 900, 64)
     shape = gc.hyq.Shape(B=1, Hq=8, Hkv=2, L=900, window=64, budget_ppm=20000, bits_kv=8)
