@@ -1,10 +1,10 @@
 // Hybrid-precision causal prefill attention: Algorithm 2, Stage 3 (App. A.2)
 // and eq. (prefill_hybrid) of Section 4.2 of HyQuant.
 //
-// One workgroup = one KV head (b, j) x one tile of 32 query rows; wave w of
-// the workgroup owns query head j*g + w (the g heads of a GQA group share
-// every K/V tile staged in LDS).  Each wave keeps one online-softmax state
-// per query row and scans
+// One workgroup = one KV head (b, j) x 8 work units, a unit being (32 query
+// rows, one query head of the group); with g = 4 that is two 32-row tiles of
+// the 4 heads.  The 8 waves (two per SIMD) share every K/V tile staged in
+// LDS.  Each wave keeps one online-softmax state per query row and scans
 //   segment A: the quantized keys (compacted K_Q order) in tiles of 64 =
 //              one quantization block: S^T = K_codes * Qcodes^T with the int8
 //              MFMA (exact int32) or, for FP8 codes, the E4M3 MFMA (float32),
@@ -57,8 +57,16 @@ typedef _Float16 v2h __attribute__((ext_vector_type(2)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
 constexpr int kTile = 64;
-constexpr int kWaves = 4;                 // waves per workgroup (one per SIMD)
+#ifndef HYQ_ATTN_WAVES
+#define HYQ_ATTN_WAVES 8
+#endif
+constexpr int kWaves = HYQ_ATTN_WAVES;    // waves per workgroup (kWaves / 4 per SIMD)
 constexpr int kThreads = kWaves * 64;
+constexpr int kWgPerCu = 8 / kWaves;      // workgroups per CU (two waves per SIMD)
+// 16-byte chunks of one staged tile: 8-bit K and V tiles are 512 chunks, 4-bit 256
+constexpr int kChunks8 = kTile * kHeadDim / 16;
+constexpr int kChunks4 = kChunks8 / 2;
+static_assert(kChunks8 % kThreads == 0, "8-bit tile chunks must split evenly");
 constexpr float kLazy = 8.0f;             // general path: rescale only when the max grows by > 2^8
 constexpr float kFastMax = 32768.0f;      // fast path: largest accepted weight sum of a lane
 constexpr float kLog2e = 1.4426950408889634f;
@@ -203,10 +211,22 @@ __device__ __forceinline__ int kswz(int row, int chunk) {
 }
 
 // (native vectors: aggregate copies of HIP's uint4 would go through memory)
+// Chunks per thread: 8-bit tiles split evenly; a 4-bit tile has one chunk for
+// each of its first 256 threads, and the other threads (if any) repeat them
+// (same data to the same LDS bytes), which keeps staging branch-free.
+template <int BITS>
+constexpr int chunks_per_thread() {
+  return BITS == 8 ? kChunks8 / kThreads : (kChunks4 >= kThreads ? kChunks4 / kThreads : 1);
+}
+template <int BITS>
+__device__ __forceinline__ int chunk_id(int tid, int i) {
+  return BITS == 8 ? tid + i * kThreads : ((tid + i * kThreads) & (kChunks4 - 1));
+}
+
 template <int BITS>
 struct StageRegs {
-  v4u k[BITS == 8 ? 2 : 1];     // 16-byte chunks tid, tid+256 of a K tile
-  v4u v[BITS == 8 ? 2 : 1];     // same for a V tile
+  v4u k[chunks_per_thread<BITS>()];   // 16-byte chunks chunk_id(tid, i) of a K tile
+  v4u v[chunks_per_thread<BITS>()];   // same for a V tile
   int32_t meta;                 // threads 0..63: kq_pos; 64, 65: sK, sV bits (K's tile)
 };
 
@@ -308,14 +328,14 @@ __device__ __forceinline__ void stage_load(StageRegs<BITS>& r, const SegA& a, in
                                            int tid) {
   constexpr int kRow = BITS == 8 ? kHeadDim : kHeadDim / 2;
   constexpr int vRow = BITS == 8 ? kTile : kTile / 2;
-  constexpr int n = BITS == 8 ? 2 : 1;
+  constexpr int n = chunks_per_thread<BITS>();
   const int t = tk;
   const v4u* kc = reinterpret_cast<const v4u*>(a.kc0 + (size_t)tk * kTile * kRow);
   const v4u* vc = reinterpret_cast<const v4u*>(a.vc0 + (size_t)tv * kHeadDim * vRow);
 #pragma unroll
-  for (int i = 0; i < n; ++i) r.k[i] = kc[tid + i * kThreads];
+  for (int i = 0; i < n; ++i) r.k[i] = kc[chunk_id<BITS>(tid, i)];
 #pragma unroll
-  for (int i = 0; i < n; ++i) r.v[i] = vc[tid + i * kThreads];
+  for (int i = 0; i < n; ++i) r.v[i] = vc[chunk_id<BITS>(tid, i)];
   // wave 0: kq_pos; wave 1: lane 0 sK, lane 1 sV; the rest reload sV
   // (choices uniform per wave or between two uniform addresses: no branch)
   const int w = tid >> 6, lane = tid & 63;
@@ -334,13 +354,13 @@ __device__ __forceinline__ void stage_store(KBuf& kb, VBuf& vb, const StageRegs<
                                             const VScale& vs) {
   if (BITS == 8) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int q = tid + i * kThreads;
+    for (int i = 0; i < chunks_per_thread<BITS>(); ++i) {
+      const int q = chunk_id<BITS>(tid, i);
       *reinterpret_cast<v4u*>(kb.k + kswz(q >> 3, q & 7)) = r.k[i];
     }
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int q = tid + i * kThreads;
+    for (int i = 0; i < chunks_per_thread<BITS>(); ++i) {
+      const int q = chunk_id<BITS>(tid, i);
       const int d = q >> 2, kg = q & 3;   // channel d, keys kg*16 .. +16
       const v4u w = r.v[i];
       uint32_t h[8];
@@ -353,8 +373,9 @@ __device__ __forceinline__ void stage_store(KBuf& kb, VBuf& vb, const StageRegs<
       *reinterpret_cast<v4u*>(dst + 16) = v4u{h[2], h[3], h[6], h[7]};
     }
   } else {
+    const int q4 = chunk_id<BITS>(tid, 0);
     {
-      const int row = tid >> 2, j4 = tid & 3;
+      const int row = q4 >> 2, j4 = q4 & 3;
       const v4u w = r.k[0];
       uint32_t o[8];
       i4x8_to_i8(w.x, o[0], o[1]);
@@ -364,7 +385,7 @@ __device__ __forceinline__ void stage_store(KBuf& kb, VBuf& vb, const StageRegs<
       *reinterpret_cast<v4u*>(kb.k + kswz(row, 2 * j4)) = v4u{o[0], o[1], o[2], o[3]};
       *reinterpret_cast<v4u*>(kb.k + kswz(row, 2 * j4 + 1)) = v4u{o[4], o[5], o[6], o[7]};
     }
-    const int d = tid >> 1, kh = tid & 1;   // channel d, keys kh*32 .. +32 (16 B packed)
+    const int d = q4 >> 1, kh = q4 & 1;   // channel d, keys kh*32 .. +32 (16 B packed)
     const v4u w = r.v[0];
     const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
@@ -575,7 +596,7 @@ __device__ __forceinline__ void segA_tile(Smem& sm, const SegA& a, int c, const 
 }
 
 template <int BITS, int OUT_BF16, int FMT>
-__global__ void __launch_bounds__(kThreads, 2)
+__global__ void __launch_bounds__(kThreads, kWgPerCu)
 attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K,
                     const uint16_t* __restrict__ V, const int32_t* __restrict__ idx,
                     const int8_t* __restrict__ q_codes, const float* __restrict__ q_scale,
@@ -591,7 +612,7 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
   const int half = lane >> 5, col = lane & 31;
 
   // Work units of one KV head: (block rb of 32 rows, query head hh of the
-  // group), ordered by rb; a workgroup takes 4 consecutive units, longest first.
+  // group), ordered by rb; a workgroup takes kWaves consecutive units, longest first.
   constexpr int kRows = 32;
   const int nrb = (L + kRows - 1) / kRows;
   const int units = g * nrb;
