@@ -418,3 +418,150 @@ def prefill(Qb, Kb, Vb, Hkv: int, W: int, budget_ppm: int, bits: int, block: int
     qz = quantize(Qb, Kb, Vb, idx, W, bits, block, fmt)
     O = attention(Qb, Kb, Vb, W, bits, idx, qz, block, heads=heads, rows=rows)
     return dict(idx=idx, O=O, **qz)
+
+
+# ---------------------------------------------------------------------------
+# Decode: Algorithm 4 (Freeze) and Algorithm 3 (HyQuant Decode)
+# ---------------------------------------------------------------------------
+#
+# Readings (the paper leaves the staging policy open):
+# * Freeze reuses the prefill steps exactly: Algorithm 1 on the prefill's
+#   tail queries, the partition, and the per-block K/V quantization over the
+#   compacted K_Q order; it keeps copies of the vertical-line rows and of the
+#   last W rows (the window) and drops the full-precision cache.
+# * The staging buffer holds up to Ws = 64 new tokens in full precision.
+#   When a new token arrives and the staging buffer is full, it is merged
+#   first: the Ws oldest window tokens are quantized as one new block of the
+#   quantized prefix (the same formula, c_B and format), and the staging
+#   tokens take their place in the window, which stays exactly W tokens.
+#   Requires W >= Ws.
+# * The decode query is used in full precision (bf16 values); quantized keys
+#   and values enter through their dequantized values s * code.  Every cached
+#   key precedes the query: there is no mask.
+
+DECODE_WS = 64
+
+
+def freeze(Qb, Kb, Vb, Hkv: int, W: int, budget_ppm: int, bits: int, block: int = 64,
+           fmt: str = "int"):
+    """Algorithm 4 on a prefill of N tokens (bf16 inputs).  Returns the hybrid
+    cache as a dict of numpy arrays (per (b, j) lists where sizes can grow):
+    quantized prefix (kq_pos, k/v codes and scales per block), vertical-line
+    rows, window rows, an empty staging buffer."""
+    if bits == 16:
+        raise ValueError("freeze needs a quantized format (bits 8 or 4)")
+    B, Hq, N, D = Qb.shape
+    idx, _ = select_vertical(Qb, Kb, Hkv, W, budget_ppm)
+    qz = quantize(Qb, Kb, Vb, idx, W, bits, block, fmt)
+    P = max(0, N - W)
+    nq = qz["kq_pos"].shape[2]
+    nb = -(-nq // block)
+    cache = dict(B=B, Hq=Hq, Hkv=Hkv, D=D, W=W, bits=bits, fmt=fmt, block=block, t=N, idx=idx)
+    kc, vc, ks, vs, pos = [], [], [], [], []
+    for b in range(B):
+        for j in range(Hkv):
+            # blocks as lists: codes [n, D] (unpacked), positions; the last Freeze
+            # block may be ragged (nq not a multiple of the block)
+            kc.append([qz["k_codes"][b, j, i * block:(i + 1) * block] for i in range(nb)])
+            vc.append([qz["v_codes"][b, j, i * block:(i + 1) * block] for i in range(nb)])
+            ks.append(list(qz["k_scale"][b, j]))
+            vs.append(list(qz["v_scale"][b, j]))
+            pos.append([qz["kq_pos"][b, j, i * block:(i + 1) * block] for i in range(nb)])
+    cache.update(k_blocks=kc, v_blocks=vc, k_scales=ks, v_scales=vs, q_pos=pos)
+    cache["vl_k"] = np.stack([Kb[b, j][idx[b, j]] for b in range(B) for j in range(Hkv)])
+    cache["vl_v"] = np.stack([Vb[b, j][idx[b, j]] for b in range(B) for j in range(Hkv)])
+    cache["vl_pos"] = idx.reshape(B * Hkv, -1)
+    # window as a list of rows per (b, j), oldest first
+    cache["win_k"] = [list(Kb[b, j][P:N]) for b in range(B) for j in range(Hkv)]
+    cache["win_v"] = [list(Vb[b, j][P:N]) for b in range(B) for j in range(Hkv)]
+    cache["win_pos"] = [list(range(P, N)) for _ in range(B * Hkv)]
+    cache["st_k"] = [[] for _ in range(B * Hkv)]
+    cache["st_v"] = [[] for _ in range(B * Hkv)]
+    cache["st_pos"] = [[] for _ in range(B * Hkv)]
+    return cache
+
+
+def _quantize_block(rows_f32: np.ndarray, cache):
+    if cache["fmt"] == "fp8":
+        return quantize_rows_fp8(rows_f32, rows_f32.shape[0])
+    return quantize_rows(rows_f32, rows_f32.shape[0], code_bound(cache["bits"]))
+
+
+def decode_merge(cache):
+    """Staging full: quantize the Ws oldest window tokens into one new block
+    of the quantized prefix; the staging tokens join the window."""
+    Ws = DECODE_WS
+    for bj in range(cache["B"] * cache["Hkv"]):
+        if cache["W"] < Ws or len(cache["st_k"][bj]) != Ws:
+            raise ValueError("merge needs W >= Ws and a full staging buffer")
+        ek = bf16_to_f32(np.stack(cache["win_k"][bj][:Ws]))
+        ev = bf16_to_f32(np.stack(cache["win_v"][bj][:Ws]))
+        kcode, ksc = _quantize_block(ek, cache)
+        vcode, vsc = _quantize_block(ev, cache)
+        cache["k_blocks"][bj].append(kcode)
+        cache["v_blocks"][bj].append(vcode)
+        cache["k_scales"][bj].append(ksc[0])
+        cache["v_scales"][bj].append(vsc[0])
+        cache["q_pos"][bj].append(np.array(cache["win_pos"][bj][:Ws], np.int32))
+        for name in ("k", "v", "pos"):
+            w, st = cache["win_" + name], cache["st_" + name]
+            w[bj] = w[bj][Ws:] + st[bj]
+            st[bj] = []
+
+
+def decode_append(cache, k_new, v_new):
+    """One new token's key and value rows (bf16 bits [B, Hkv, D]) enter the
+    staging buffer (merging it first if it is full)."""
+    if len(cache["st_k"][0]) == DECODE_WS:
+        decode_merge(cache)
+    t = cache["t"]
+    for b in range(cache["B"]):
+        for j in range(cache["Hkv"]):
+            bj = b * cache["Hkv"] + j
+            cache["st_k"][bj].append(np.asarray(k_new[b, j]))
+            cache["st_v"][bj].append(np.asarray(v_new[b, j]))
+            cache["st_pos"][bj].append(t)
+    cache["t"] = t + 1
+
+
+def decode_keys(cache, bj):
+    """Every cached key of KV head bj with its value and original position:
+    (K [n, D] float64, V [n, D] float64, pos [n]); quantized keys dequantized
+    as scale * value(code)."""
+    fmt = cache["fmt"]
+    Ks, Vs, Ps = [], [], []
+    for kc, vc, ksc, vsc, pos in zip(cache["k_blocks"][bj], cache["v_blocks"][bj],
+                                     cache["k_scales"][bj], cache["v_scales"][bj],
+                                     cache["q_pos"][bj]):
+        n = len(pos)
+        Ks.append(np.float64(ksc) * code_values(kc[:n], fmt))
+        Vs.append(np.float64(vsc) * code_values(vc[:n], fmt))
+        Ps.append(np.asarray(pos, np.int64))
+    for kk, vv, pp in ((cache["vl_k"][bj], cache["vl_v"][bj], cache["vl_pos"][bj]),
+                       (cache["win_k"][bj], cache["win_v"][bj], cache["win_pos"][bj]),
+                       (cache["st_k"][bj], cache["st_v"][bj], cache["st_pos"][bj])):
+        if len(pp):
+            Ks.append(bf16_to_f32(np.stack(kk)).astype(np.float64))
+            Vs.append(bf16_to_f32(np.stack(vv)).astype(np.float64))
+            Ps.append(np.asarray(pp, np.int64))
+    return np.concatenate(Ks), np.concatenate(Vs), np.concatenate(Ps)
+
+
+def decode_attention(q_bits, cache):
+    """Algorithm 3 for one decode query per (batch, query head): softmax of
+    alpha * q . k over every cached key (float64, one plain row-wise softmax),
+    times the values; returns O [B, Hq, D] float32."""
+    B, Hq, Hkv, D = cache["B"], cache["Hq"], cache["Hkv"], cache["D"]
+    g = Hq // Hkv
+    alpha = 1.0 / math.sqrt(D)
+    q = bf16_to_f32(q_bits).astype(np.float64)
+    O = np.zeros((B, Hq, D), np.float32)
+    for b in range(B):
+        for j in range(Hkv):
+            Kall, Vall, _ = decode_keys(cache, b * Hkv + j)
+            for r in range(g):
+                h = j * g + r
+                z = alpha * (Kall @ q[b, h])
+                e = np.exp(z - z.max())
+                O[b, h] = ((e @ Vall) / e.sum()).astype(np.float32)
+    return O
