@@ -166,6 +166,127 @@ HYQ_API int hyq_attn_prefill(const hyq_shape* shape, const void* Q, const void* 
                      const int32_t* kq_pos, float softmax_scale,
                      void* out, int32_t out_dtype, void* stream);
 
+/* ======================================================================
+ * Decode: Algorithm 4 (Freeze, App. A.4) and Algorithm 3 (HyQuant Decode,
+ * App. A.3).
+ *
+ * Freeze turns a prefill of N tokens into the hybrid KV cache of decode:
+ *   - vertical-line tokens (Algorithm 1 on the prefill's tail queries, held
+ *     fixed from then on): K and V kept in bf16;
+ *   - the other non-window tokens [0, N-W) minus the vertical lines:
+ *     per-block quantized exactly as hyq_quantize quantizes K_Q and V_Q;
+ *   - the last W tokens (the window): kept in bf16;
+ *   - an empty staging buffer of HYQ_DECODE_WS tokens, kept in bf16.
+ * Each decode step appends one token.  When it arrives with the staging
+ * buffer full, the HYQ_DECODE_WS oldest window tokens are first quantized
+ * into one new block of the quantized prefix (same formula, c_B and format)
+ * and the staged tokens join the window, which stays W tokens long.
+ * Decode attention of one query row per (b, h) is one softmax over every
+ * cached key (no mask): quantized keys enter as scale * code, all other
+ * keys as their bf16 values; the query is used in full precision.
+ *
+ * Memory: the window and the staging buffer share one ring of
+ * ring_rows = roundup(W, 64) + 64 bf16 rows per KV head (window = the W
+ * oldest valid rows from ring_head on, staging = the rest), so a merge
+ * moves no full-precision data.  Vertical-line rows and the ring are stored
+ * together: fp_k row i < vl_rows is vertical line i (rows >= n_vl are zero
+ * padding), row vl_rows + s is ring slot s.  fp_v holds the same rows
+ * transposed (channel-major), the layout the P.V matrix product reads.
+ * The caller owns every buffer; state lives in the struct, which
+ * hyq_decode_append advances on the host.
+ * ==================================================================== */
+
+#define HYQ_DECODE_WS 64   /* staging buffer capacity W_s (tokens)            */
+
+typedef struct hyq_dcache {
+  /* geometry, set by hyq_dcache_init */
+  int32_t B, Hq, Hkv, D;
+  int32_t window;        /* W, 64 <= W <= N                                      */
+  int32_t bits_kv;       /* 8 or 4                                               */
+  int32_t kv_format;     /* HYQ_FMT_INT or HYQ_FMT_FP8                           */
+  int32_t n_vl;          /* k: vertical-line tokens per KV head                  */
+  int32_t vl_rows;       /* k rounded up to a multiple of 64                     */
+  int32_t ring_rows;     /* roundup(W, 64) + HYQ_DECODE_WS                       */
+  int32_t n_frozen;      /* quantized tokens written by Freeze (nQ of the prefill)*/
+  int32_t cap_blocks;    /* quantized blocks the buffers hold (Freeze + merges)  */
+  /* state, set by hyq_freeze and advanced by hyq_decode_append */
+  int32_t n_merged;      /* merged blocks, stored after the ceil(nQ/64) frozen ones */
+  int32_t ring_head;     /* ring slot of the oldest window token                 */
+  int32_t n_staged;      /* tokens in the staging buffer, 0..HYQ_DECODE_WS       */
+  int32_t reserved;
+  int64_t t;             /* tokens cached: N + appended tokens                   */
+  /* caller-owned device buffers (byte sizes from hyq_dcache_init) */
+  void* k_codes;         /* [B][Hkv][cap_blocks*64][row] row-major, as hyq_quantize */
+  void* v_codes;         /* [B][Hkv][cap_blocks][D][64*bits/8] channel-major blocks */
+  float* k_scale;        /* [B][Hkv][cap_blocks]                                 */
+  float* v_scale;        /* [B][Hkv][cap_blocks]                                 */
+  int32_t* q_pos;        /* [B][Hkv][cap_blocks*64]: original position of each
+                            quantized token; HYQ_KQ_POS_PAD in padding slots     */
+  void* fp_k;            /* bf16 [B][Hkv][vl_rows + ring_rows][D]                */
+  void* fp_v;            /* bf16 [B][Hkv][D][vl_rows + ring_rows]                */
+  int32_t* vl_pos;       /* [B][Hkv][n_vl]: vertical-line positions, ascending   */
+} hyq_dcache;
+
+typedef struct hyq_dcache_sizes {
+  size_t k_codes_bytes, v_codes_bytes, k_scale_bytes, v_scale_bytes, q_pos_bytes;
+  size_t fp_k_bytes, fp_v_bytes, vl_pos_bytes;
+  size_t freeze_ws_bytes;   /* workspace of hyq_freeze                              */
+  size_t attn_ws_bytes;     /* workspace of hyq_decode_attn (any state of the cache)*/
+} hyq_dcache_sizes;
+
+/*
+ * Pure host arithmetic: fills the geometry of a decode cache for a prefill
+ * of shape `prefill` (L = N tokens; window, budget, bits and format as for
+ * the prefill calls; bits_kv must be 8 or 4) that will hold up to
+ * max_tokens tokens (>= N), zeroes its state and buffer pointers, and
+ * returns the byte size of every buffer.
+ * Errors: HYQ_EINVAL if W < HYQ_DECODE_WS, N < W or max_tokens < N.
+ */
+HYQ_API int hyq_dcache_init(const hyq_shape* prefill, int64_t max_tokens, hyq_dcache* cache,
+                            hyq_dcache_sizes* sizes);
+
+/*
+ * Algorithm 4 (Freeze).  Q, K, V: the prefill's bf16 tensors (shape as for
+ * the prefill calls); only the last min(W, N) query rows are read.  Fills
+ * every buffer of `cache` (whose pointers the caller has set) and sets its
+ * state: no merged blocks, ring_head 0, nothing staged, t = N.
+ * ws: device workspace of at least freeze_ws_bytes (scratch).
+ */
+HYQ_API int hyq_freeze(const hyq_shape* prefill, const void* Q, const void* K, const void* V,
+                       hyq_dcache* cache, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * One decode step's key and value rows, k_new and v_new bf16 [B][Hkv][D],
+ * enter the staging buffer; when the staging buffer is full they are
+ * preceded by the merge of the HYQ_DECODE_WS oldest window tokens into
+ * quantized block ceil(n_frozen/64) + n_merged.  Advances the state in
+ * `cache` (host memory).
+ * Errors: HYQ_EINVAL when a merge is due and all cap_blocks blocks are in
+ * use (nothing is enqueued and the state is unchanged).
+ */
+HYQ_API int hyq_decode_append(hyq_dcache* cache, const void* k_new, const void* v_new,
+                              void* stream);
+
+/*
+ * Algorithm 3: attention of one query row per (b, h) over every token of
+ * the cache, split over the sequence axis and merged as in its
+ * ReduceSoftmax step:
+ *   out[b][h] = sum_k w_k value_k / sum_k w_k,  w_k = exp(z_k - max z),
+ *   z_k = alpha * <q[b][h], key_k>, with key/value = scale * code for
+ *   quantized tokens and the bf16 rows for vertical-line, window and staged
+ *   tokens.  alpha = softmax_scale.
+ * q: bf16 [B][Hq][D]; out: [B][Hq][D], float32 (out_dtype 0) or bf16 (1).
+ * ws: device workspace of at least attn_ws_bytes (scratch).
+ * Precision: the query enters the products with quantized keys as f16
+ * after an exact power-of-two scaling per head (exact unless an entry is
+ * below 2^-29 of the head's largest), codes as exact f16; full-precision
+ * keys as bf16 x bf16; float32 accumulation; weights as f16 against
+ * quantized values and as a high + low bf16 pair against bf16 values.
+ */
+HYQ_API int hyq_decode_attn(const hyq_dcache* cache, const void* q, float softmax_scale,
+                            void* out, int32_t out_dtype, void* ws, size_t ws_bytes,
+                            void* stream);
+
 /* Static description of a return code. */
 HYQ_API const char* hyq_strerror(int code);
 

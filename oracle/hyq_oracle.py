@@ -434,7 +434,8 @@ def prefill(Qb, Kb, Vb, Hkv: int, W: int, budget_ppm: int, bits: int, block: int
 #   first: the Ws oldest window tokens are quantized as one new block of the
 #   quantized prefix (the same formula, c_B and format), and the staging
 #   tokens take their place in the window, which stays exactly W tokens.
-#   Requires W >= Ws.
+#   Requires W >= Ws, and a prefill of N >= W tokens (so that the window is
+#   full from the start).
 # * The decode query is used in full precision (bf16 values); quantized keys
 #   and values enter through their dequantized values s * code.  Every cached
 #   key precedes the query: there is no mask.
@@ -451,6 +452,8 @@ def freeze(Qb, Kb, Vb, Hkv: int, W: int, budget_ppm: int, bits: int, block: int 
     if bits == 16:
         raise ValueError("freeze needs a quantized format (bits 8 or 4)")
     B, Hq, N, D = Qb.shape
+    if W < DECODE_WS or N < W:
+        raise ValueError("decode needs W >= Ws (merges move Ws window tokens) and N >= W")
     idx, _ = select_vertical(Qb, Kb, Hkv, W, budget_ppm)
     qz = quantize(Qb, Kb, Vb, idx, W, bits, block, fmt)
     P = max(0, N - W)

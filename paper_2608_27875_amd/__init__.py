@@ -1,5 +1,6 @@
 """Python binding of libhyq, the MI355X (gfx950) HyQuant hybrid-precision
-prefill attention library.
+attention library (prefill operator, and the decode cache with its
+attention).
 
 The functions here carry the C ABI's names (``include/hyq.h``) and only
 marshal arguments: torch tensors (device memory) become pointers, the
@@ -22,8 +23,10 @@ LIB_PATH = os.path.join(_HERE, "libhyq.so")
 HYQ_OK, HYQ_EINVAL, HYQ_EUNSUPPORTED, HYQ_EHIP = 0, -1, -2, -3
 KQ_POS_PAD = 0x7FFFFFFF
 FMT_INT, FMT_FP8 = 0, 1       # hyq_shape.kv_format
+DECODE_WS = 64                # HYQ_DECODE_WS: staging buffer capacity
 EXPORTED = ("hyq_sizes_for", "hyq_select_vertical", "hyq_quantize", "hyq_attn_prefill",
-            "hyq_strerror", "hyq_last_error")
+            "hyq_strerror", "hyq_last_error", "hyq_dcache_init", "hyq_freeze",
+            "hyq_decode_append", "hyq_decode_attn")
 
 
 class HyqError(RuntimeError):
@@ -43,6 +46,25 @@ class _Sizes(ctypes.Structure):
                [(n, ctypes.c_size_t) for n in ("idx_bytes", "kq_pos_bytes", "q_codes_bytes",
                                                "q_scale_bytes", "k_codes_bytes", "v_codes_bytes",
                                                "kv_scale_bytes", "scores_bytes", "select_ws_bytes")]
+
+
+_DCACHE_INTS = ("B", "Hq", "Hkv", "D", "window", "bits_kv", "kv_format", "n_vl", "vl_rows",
+                "ring_rows", "n_frozen", "cap_blocks", "n_merged", "ring_head", "n_staged",
+                "reserved")
+_DCACHE_PTRS = ("k_codes", "v_codes", "k_scale", "v_scale", "q_pos", "fp_k", "fp_v", "vl_pos")
+
+
+class _DCache(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in _DCACHE_INTS] + [("t", ctypes.c_int64)] + \
+               [(n, ctypes.c_void_p) for n in _DCACHE_PTRS]
+
+
+_DSIZES = ("k_codes_bytes", "v_codes_bytes", "k_scale_bytes", "v_scale_bytes", "q_pos_bytes",
+           "fp_k_bytes", "fp_v_bytes", "vl_pos_bytes", "freeze_ws_bytes", "attn_ws_bytes")
+
+
+class _DCacheSizes(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_size_t) for n in _DSIZES]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -85,7 +107,15 @@ def lib():
         L.hyq_strerror.argtypes = [ctypes.c_int]
         L.hyq_last_error.restype = ctypes.c_char_p
         L.hyq_last_error.argtypes = []
-        for f in ("hyq_sizes_for", "hyq_select_vertical", "hyq_quantize", "hyq_attn_prefill"):
+        DC = ctypes.POINTER(_DCache)
+        L.hyq_dcache_init.argtypes = [ctypes.POINTER(_Shape), ctypes.c_int64, DC,
+                                      ctypes.POINTER(_DCacheSizes)]
+        L.hyq_freeze.argtypes = [ctypes.POINTER(_Shape), P, P, P, DC, P, ctypes.c_size_t, P]
+        L.hyq_decode_append.argtypes = [DC, P, P, P]
+        L.hyq_decode_attn.argtypes = [DC, P, ctypes.c_float, P, ctypes.c_int32, P,
+                                      ctypes.c_size_t, P]
+        for f in ("hyq_sizes_for", "hyq_select_vertical", "hyq_quantize", "hyq_attn_prefill",
+                  "hyq_dcache_init", "hyq_freeze", "hyq_decode_append", "hyq_decode_attn"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -273,3 +303,109 @@ def prefill(shape: Shape, Q, K, V, bufs: dict, out_dtype: int = 0, stream=None,
                      b["k_scale"], b["v_codes"], b["v_scale"], b["kq_pos"], scale, b["out"],
                      out_dtype, stream)
     return b["out"]
+
+
+# --------------------------------------------------------------------------
+# decode: Algorithm 4 (Freeze) and Algorithm 3 (decode attention)
+# --------------------------------------------------------------------------
+
+def hyq_dcache_init(shape: Shape, max_tokens: int):
+    """Geometry of the decode cache of a prefill (see include/hyq.h):
+    returns (ctypes hyq_dcache with NULL buffers, dict of buffer sizes)."""
+    c = _DCache()
+    z = _DCacheSizes()
+    _check(lib().hyq_dcache_init(ctypes.byref(shape.c()), ctypes.c_int64(max_tokens),
+                                 ctypes.byref(c), ctypes.byref(z)))
+    return c, {n: getattr(z, n) for n in _DSIZES}
+
+
+class DecodeCache:
+    """A hybrid KV cache on one device: the ``hyq_dcache`` struct (geometry
+    and host-side state) and the torch tensors that own its buffers."""
+
+    def __init__(self, shape: Shape, max_tokens: int, device):
+        torch = _torch()
+        self.shape = shape
+        self.c, self.sizes = hyq_dcache_init(shape, max_tokens)
+        dev = torch.device(device)
+        if dev.type == "cuda" and dev.index is None:
+            dev = torch.device("cuda", torch.cuda.current_device())
+        self.device = dev
+        z = self.sizes
+
+        def u8(n):
+            return torch.zeros(max(n, 1), dtype=torch.uint8, device=self.device)
+
+        self.bufs = {
+            "k_codes": u8(z["k_codes_bytes"]), "v_codes": u8(z["v_codes_bytes"]),
+            "k_scale": torch.zeros(max(z["k_scale_bytes"] // 4, 1), dtype=torch.float32,
+                                   device=self.device),
+            "v_scale": torch.zeros(max(z["v_scale_bytes"] // 4, 1), dtype=torch.float32,
+                                   device=self.device),
+            "q_pos": torch.zeros(max(z["q_pos_bytes"] // 4, 1), dtype=torch.int32,
+                                 device=self.device),
+            "fp_k": torch.zeros(max(z["fp_k_bytes"] // 2, 1), dtype=torch.bfloat16,
+                                device=self.device),
+            "fp_v": torch.zeros(max(z["fp_v_bytes"] // 2, 1), dtype=torch.bfloat16,
+                                device=self.device),
+            "vl_pos": torch.zeros(max(z["vl_pos_bytes"] // 4, 1), dtype=torch.int32,
+                                  device=self.device),
+        }
+        for n in _DCACHE_PTRS:
+            t = self.bufs[n]
+            have = t.numel() * t.element_size()
+            if have < z[n + "_bytes"]:
+                raise ValueError(f"{n}: {have} bytes < {z[n + '_bytes']}")
+            setattr(self.c, n, t.data_ptr())
+        self.freeze_ws = u8(z["freeze_ws_bytes"])
+        self.attn_ws = u8(z["attn_ws_bytes"])
+
+    @property
+    def state(self) -> dict:
+        return {n: getattr(self.c, n) for n in ("n_merged", "ring_head", "n_staged", "t")}
+
+    def geometry(self) -> dict:
+        return {n: getattr(self.c, n) for n in _DCACHE_INTS if n != "reserved"}
+
+
+def _decode_rows_ok(cache: DecodeCache, t, name, heads):
+    torch = _torch()
+    want = (cache.c.B, heads, cache.c.D)
+    if tuple(t.shape) != want:
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {want}")
+    return _ptr(t, name, t.numel() * 2, (torch.bfloat16,), cache.device)
+
+
+def hyq_freeze(shape: Shape, Q, K, V, cache: DecodeCache, stream=None):
+    """Algorithm 4: fill ``cache`` from the prefill's bf16 Q, K, V."""
+    dev, bf = _io(shape, Q, K, V)
+    if dev != cache.device:
+        raise ValueError("Q, K, V must be on the cache's device")
+    a = [_ptr(Q, "Q", Q.numel() * 2, bf, dev), _ptr(K, "K", K.numel() * 2, bf, dev),
+         _ptr(V, "V", V.numel() * 2, bf, dev)]
+    ws = cache.freeze_ws
+    _check(lib().hyq_freeze(ctypes.byref(shape.c()), *a, ctypes.byref(cache.c),
+                            ctypes.c_void_p(ws.data_ptr()),
+                            ctypes.c_size_t(ws.numel()), _stream(stream)))
+
+
+def hyq_decode_append(cache: DecodeCache, k_new, v_new, stream=None):
+    """One decode step's K and V rows (bf16 [B, Hkv, D]) into the cache."""
+    k = _decode_rows_ok(cache, k_new, "k_new", cache.c.Hkv)
+    v = _decode_rows_ok(cache, v_new, "v_new", cache.c.Hkv)
+    _check(lib().hyq_decode_append(ctypes.byref(cache.c), k, v, _stream(stream)))
+
+
+def hyq_decode_attn(cache: DecodeCache, q, out, softmax_scale: float | None = None,
+                    out_dtype: int = 0, stream=None):
+    """Algorithm 3: out[b, h] = attention of q[b, h] (bf16 [B, Hq, D]) over the cache."""
+    torch = _torch()
+    qp = _decode_rows_ok(cache, q, "q", cache.c.Hq)
+    scale = 1.0 / math.sqrt(cache.c.D) if softmax_scale is None else softmax_scale
+    odt = (torch.float32,) if out_dtype == 0 else (torch.bfloat16,)
+    nb = cache.c.B * cache.c.Hq * cache.c.D * (4 if out_dtype == 0 else 2)
+    o = _ptr(out, "out", nb, odt, cache.device)
+    ws = cache.attn_ws
+    _check(lib().hyq_decode_attn(ctypes.byref(cache.c), qp, ctypes.c_float(scale), o,
+                                 ctypes.c_int32(out_dtype), ctypes.c_void_p(ws.data_ptr()),
+                                 ctypes.c_size_t(ws.numel()), _stream(stream)))

@@ -1,0 +1,780 @@
+// Decode path of HyQuant (Section 4.3): Freeze (Algorithm 4, App. A.4), the
+// staging buffer and its merges into the quantized prefix, and the decode
+// attention of Algorithm 3 (App. A.3): the quantized prefix split along the
+// sequence axis, every split an online softmax, the splits and the
+// full-precision segments merged by ReduceSoftmax.
+//
+// Decode attention is bound by HBM bandwidth: every cached byte is read once
+// per step and each key meets only g = Hq/Hkv query rows.  The kernel is laid
+// out so that each byte goes from HBM straight into an MFMA operand register
+// with no LDS round trip:
+//   - one wave owns whole 64-token units (a quantization block, or a tile of
+//     64 full-precision rows) and keeps its own online-softmax state;
+//   - S^T = K q^T with the 16x16x32 MFMA (keys as rows, the g heads of the
+//     KV group as columns, padded to 16): the A operand is read directly from
+//     the row-major K codes (one 16-byte load per lane and 16 keys);
+//   - the accumulator layout of S^T (lane l: head l%16, keys
+//     (l/16)*16 + 4t + r of the unit for tile t, register r) is exactly the
+//     B operand layout of O^T = V^T P^T, and the channel-major V codes of a
+//     block are exactly its A operand, so P never leaves registers and V is
+//     never transposed on chip;
+//   - quantized codes become exact f16 MFMA operands (codes_dev.h); the
+//     query enters as f16 after an exact power-of-two scaling per head;
+//     full-precision tiles use the bf16 MFMA with P as a high + low bf16
+//     pair.
+// A workgroup (4 waves) merges its waves' states in LDS and writes one
+// partial (m, l, acc) per query head; a second kernel reduces the partials.
+#include "codes_dev.h"
+#include "hyq_internal.h"
+#include "quant_dev.h"
+
+#include <type_traits>
+
+namespace hyq {
+namespace {
+
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+typedef unsigned v2u __attribute__((ext_vector_type(2)));
+
+constexpr int kDecWaves = 4;
+constexpr int kDecThreads = kDecWaves * 64;
+constexpr int kPartStride = 132;           // floats per partial: acc[128], m, l, pad
+constexpr float kLazyD = 8.0f;             // rescale only when the max grows by > 2^8
+constexpr float kMinusBigD = -1.0e30f;
+constexpr int kMaxGroup = 8;
+
+// ---------------------------------------------------------------------------
+// Freeze: gather the vertical-line rows and the window into the bf16 rows of
+// the cache (K row-major, V channel-major); every other row is zeroed.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256)
+freeze_gather_kernel(const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
+                     const int32_t* __restrict__ idx, uint16_t* __restrict__ fk,
+                     uint16_t* __restrict__ fv, int N, int W, int k, int vl_rows, int nfp) {
+  __shared__ uint16_t tile[kBlock][kHeadDim + 2];
+  const int bj = blockIdx.y;
+  const int row = threadIdx.x >> 2, c0 = (threadIdx.x & 3) * 32;
+  const int i = blockIdx.x * kBlock + row;
+  int src = -1;
+  if (i < k) src = idx[(size_t)bj * k + i];
+  else if (i >= vl_rows && i - vl_rows < W) src = N - W + (i - vl_rows);
+  v4u kw[4], vw[4];
+  if (src >= 0) {
+    const v4u* kp = reinterpret_cast<const v4u*>(K + ((size_t)bj * N + src) * kHeadDim + c0);
+    const v4u* vp = reinterpret_cast<const v4u*>(V + ((size_t)bj * N + src) * kHeadDim + c0);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      kw[u] = kp[u];
+      vw[u] = vp[u];
+    }
+  } else {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) kw[u] = vw[u] = v4u{0u, 0u, 0u, 0u};
+  }
+  v4u* kd = reinterpret_cast<v4u*>(fk + ((size_t)bj * nfp + i) * kHeadDim + c0);
+#pragma unroll
+  for (int u = 0; u < 4; ++u) kd[u] = kw[u];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      tile[row][c0 + u * 8 + 2 * e] = (uint16_t)(vw[u][e] & 0xffffu);
+      tile[row][c0 + u * 8 + 2 * e + 1] = (uint16_t)(vw[u][e] >> 16);
+    }
+  }
+  __syncthreads();
+  // transposed write: thread -> (channel d, 32 rows)
+  const int d = threadIdx.x >> 1, r0 = (threadIdx.x & 1) * 32;
+  v4u o[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      o[u][e] = (uint32_t)tile[r0 + u * 8 + 2 * e][d] |
+                ((uint32_t)tile[r0 + u * 8 + 2 * e + 1][d] << 16);
+  v4u* vd = reinterpret_cast<v4u*>(fv + ((size_t)bj * kHeadDim + d) * nfp +
+                                   (size_t)blockIdx.x * kBlock + r0);
+#pragma unroll
+  for (int u = 0; u < 4; ++u) vd[u] = o[u];
+}
+
+// ---------------------------------------------------------------------------
+// Append one token (and, first, merge the 64 oldest window tokens into a new
+// quantized block when the staging buffer is full).  blockIdx.y = 0: K,
+// 1: V; one workgroup per (b, j).
+// ---------------------------------------------------------------------------
+struct AppendArgs {
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  uint16_t* fk;
+  uint16_t* fv;
+  uint8_t* kc;
+  uint8_t* vc;
+  float* ks;
+  float* vs;
+  int32_t* q_pos;
+  int nfp, vl_rows, ring_rows, W;
+  int merge;          // 1: quantize ring slots [head, head + 64) into block `blk`
+  int head;           // ring head before the merge
+  int blk;            // block index of the merged block
+  int cap_blocks;
+  int pos0;           // original position of the oldest window token
+  int slot;           // ring slot the new token goes to
+};
+
+template <int BITS, int FMT>
+__global__ void __launch_bounds__(kQuantThreads)
+append_kernel(AppendArgs a) {
+  constexpr float C = FMT == HYQ_FMT_FP8 ? 448.0f : (BITS == 8 ? 127.0f : 7.0f);
+  constexpr int kRow = BITS == 8 ? kHeadDim : kHeadDim / 2;
+  constexpr int vRow = BITS == 8 ? kBlock : kBlock / 2;
+  __shared__ float red[kQuantThreads / 64];
+  const int bj = blockIdx.x;
+  const bool is_v = blockIdx.y == 1;
+  if (a.merge) {
+    float x[32];
+    if (!is_v) {
+      const int row = threadIdx.x >> 2, c0 = (threadIdx.x & 3) * 32;
+      const int slot = (a.head + row) % a.ring_rows;
+      load32(a.fk + ((size_t)bj * a.nfp + a.vl_rows + slot) * kHeadDim + c0, x);
+      float m = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) m = fmaxf(m, fabsf(x[e]));
+      const float s = block_max(m, red) / C;
+      uint8_t* dst = a.kc + ((size_t)bj * a.cap_blocks * kBlock + (size_t)a.blk * kBlock + row) * kRow;
+      if (BITS == 8) {
+        v4u w[2];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          uint32_t v = 0;
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            v |= (uint32_t)((s > 0.0f ? quant_code<FMT>(x[4 * e + q], s, C) : 0) & 0xff) << (8 * q);
+          w[e >> 2][e & 3] = v;
+        }
+        v4u* d4 = reinterpret_cast<v4u*>(dst + c0);
+        d4[0] = w[0];
+        d4[1] = w[1];
+      } else {
+        v4u w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          uint32_t v = 0;
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            v |= (uint32_t)((s > 0.0f ? quant_code<FMT>(x[8 * e + q], s, C) : 0) & 0xf) << (4 * q);
+          w[e] = v;
+        }
+        *reinterpret_cast<v4u*>(dst + c0 / 2) = w;
+      }
+      if (threadIdx.x == 0) a.ks[(size_t)bj * a.cap_blocks + a.blk] = s;
+      if ((threadIdx.x & 3) == 0)
+        a.q_pos[(size_t)bj * a.cap_blocks * kBlock + (size_t)a.blk * kBlock + row] = a.pos0 + row;
+    } else {
+      // V rows are stored channel-major: thread -> (channel d, 32 tokens)
+      const int d = threadIdx.x >> 1, r0 = (threadIdx.x & 1) * 32;
+      const uint16_t* src = a.fv + ((size_t)bj * kHeadDim + d) * a.nfp + a.vl_rows;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) x[e] = bf16_bits_to_f32(src[(a.head + r0 + e) % a.ring_rows]);
+      float m = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) m = fmaxf(m, fabsf(x[e]));
+      const float s = block_max(m, red) / C;
+      uint8_t* dst = a.vc + (((size_t)bj * a.cap_blocks + a.blk) * kHeadDim + d) * vRow;
+      if (BITS == 8) {
+        v4u w[2];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          uint32_t v = 0;
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            v |= (uint32_t)((s > 0.0f ? quant_code<FMT>(x[4 * e + q], s, C) : 0) & 0xff) << (8 * q);
+          w[e >> 2][e & 3] = v;
+        }
+        v4u* d4 = reinterpret_cast<v4u*>(dst + r0);
+        d4[0] = w[0];
+        d4[1] = w[1];
+      } else {
+        v4u w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          uint32_t v = 0;
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            v |= (uint32_t)((s > 0.0f ? quant_code<FMT>(x[8 * e + q], s, C) : 0) & 0xf) << (4 * q);
+          w[e] = v;
+        }
+        *reinterpret_cast<v4u*>(dst + r0 / 2) = w;
+      }
+      if (threadIdx.x == 0) a.vs[(size_t)bj * a.cap_blocks + a.blk] = s;
+    }
+    __syncthreads();   // the new token may take a slot the merge has just read
+  }
+  if (!is_v) {
+    if (threadIdx.x < 16) {
+      const v4u* s = reinterpret_cast<const v4u*>(a.k_new + (size_t)bj * kHeadDim);
+      v4u* d = reinterpret_cast<v4u*>(a.fk + ((size_t)bj * a.nfp + a.vl_rows + a.slot) * kHeadDim);
+      d[threadIdx.x] = s[threadIdx.x];
+    }
+  } else if (threadIdx.x < kHeadDim) {
+    a.fv[((size_t)bj * kHeadDim + threadIdx.x) * a.nfp + a.vl_rows + a.slot] =
+        a.v_new[(size_t)bj * kHeadDim + threadIdx.x];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Decode attention.
+// ---------------------------------------------------------------------------
+struct DecodeArgs {
+  const uint8_t* kc;
+  const uint8_t* vc;
+  const float* ks;
+  const float* vs;
+  const uint16_t* fk;
+  const uint16_t* fv;
+  const uint16_t* q;
+  float* part;
+  int Hq, Hkv, g;
+  int cap_blocks;
+  int nbq;          // quantized blocks in use (frozen + merged)
+  int nbf;          // frozen blocks; block nbf-1 holds n_last tokens
+  int n_last;
+  int n_vl, vl_rows, nfp, ring_head, ring_rows, ring_valid;
+  int S_q, S_f, U;  // quantized splits, full-precision splits, blocks per wave
+  float c_log2;     // softmax_scale * log2(e)
+};
+
+// Packed int4 codes (nibble n = element n, two's complement) -> f16 values
+// code * 2^e in the element order [0, 4, 1, 5, 2, 6, 3, 7]: each nibble,
+// biased by 8, is placed in the low mantissa bits of 1024 (f16 0x6400),
+// either at bit 0 (value 1024 + u) or at bit 4 (1024 + 16 u), and one fused
+// multiply-add per pair removes the offset and applies 2^e.  Exact.
+struct I4Scale {
+  v2h m1, b1, m16, b16;
+};
+__device__ __forceinline__ I4Scale make_i4scale(float p2) {
+  I4Scale s;
+  const _Float16 a = (_Float16)p2, b = (_Float16)(-1032.0f * p2);
+  const _Float16 c = (_Float16)(p2 * 0.0625f), d = (_Float16)(-72.0f * p2);
+  s.m1 = v2h{a, a};
+  s.b1 = v2h{b, b};
+  s.m16 = v2h{c, c};
+  s.b16 = v2h{d, d};
+  return s;
+}
+__device__ __forceinline__ v8h i4x8_to_h_perm(uint32_t w, const I4Scale& s) {
+  const uint32_t u = w ^ 0x88888888u;
+  const uint32_t u8 = u >> 8;
+  const v2h a = __builtin_bit_cast(v2h, (u & 0x000F000Fu) | 0x64006400u);
+  const v2h b = __builtin_bit_cast(v2h, (u & 0x00F000F0u) | 0x64006400u);
+  const v2h c = __builtin_bit_cast(v2h, (u8 & 0x000F000Fu) | 0x64006400u);
+  const v2h d = __builtin_bit_cast(v2h, (u8 & 0x00F000F0u) | 0x64006400u);
+  const v2h ha = __builtin_elementwise_fma(a, s.m1, s.b1);    // elements 0, 4
+  const v2h hb = __builtin_elementwise_fma(b, s.m16, s.b16);  // elements 1, 5
+  const v2h hc = __builtin_elementwise_fma(c, s.m1, s.b1);    // elements 2, 6
+  const v2h hd = __builtin_elementwise_fma(d, s.m16, s.b16);  // elements 3, 7
+  return v8h{ha[0], ha[1], hb[0], hb[1], hc[0], hc[1], hd[0], hd[1]};
+}
+
+// 8 one-byte codes (two dwords) -> f16 values code * 2^e, element order.
+template <int FMT>
+__device__ __forceinline__ v8h b8x8_to_h(uint32_t w0, uint32_t w1, const VScale& vs) {
+  uint32_t h[4];
+  codes4_to_h<FMT>(w0, h[0], h[1], vs);
+  codes4_to_h<FMT>(w1, h[2], h[3], vs);
+  return __builtin_bit_cast(v8h, v4u{h[0], h[1], h[2], h[3]});
+}
+
+// Per-block code registers of one wave: K rows of the 4 MFMA tiles, V^T rows
+// of the 8 channel tiles.
+template <int BITS>
+struct QRegs {
+  static constexpr int kK = BITS == 8 ? 2 : 1;   // 16-byte loads per K tile
+  v4u k[4][kK];
+  typename std::conditional<BITS == 8, v4u, v2u>::type v[8];
+};
+
+// Row of the unit read by MFMA tile t, A-operand row m: (m/4)*16 + 4t + m%4,
+// so that accumulator register r of lane l holds key (l/16)*16 + 4t + r.
+__device__ __forceinline__ int unit_row(int t, int m) { return ((m >> 2) << 4) + (t << 2) + (m & 3); }
+
+template <int BITS>
+__device__ __forceinline__ void load_block(QRegs<BITS>& r, const DecodeArgs& a, int bj, int blk,
+                                           int hl, int G) {
+  constexpr int kRow = BITS == 8 ? kHeadDim : kHeadDim / 2;
+  constexpr int vRow = BITS == 8 ? kBlock : kBlock / 2;
+  const uint8_t* kb = a.kc + ((size_t)bj * a.cap_blocks + blk) * kBlock * kRow;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const v4u* p = reinterpret_cast<const v4u*>(kb + unit_row(t, hl) * kRow + G * (kRow / 4));
+#pragma unroll
+    for (int u = 0; u < QRegs<BITS>::kK; ++u) r.k[t][u] = __builtin_nontemporal_load(p + u);
+  }
+  const uint8_t* vb = a.vc + ((size_t)bj * a.cap_blocks + blk) * kHeadDim * vRow;
+#pragma unroll
+  for (int ct = 0; ct < 8; ++ct) {
+    const uint8_t* p = vb + (ct * 16 + hl) * vRow + G * (vRow / 4);
+    if constexpr (BITS == 8) r.v[ct] = __builtin_nontemporal_load(reinterpret_cast<const v4u*>(p));
+    else r.v[ct] = __builtin_nontemporal_load(reinterpret_cast<const v2u*>(p));
+  }
+}
+
+__device__ __forceinline__ float xgroup_max(float x) {
+  x = fmaxf(x, __shfl_xor(x, 16, 64));
+  return fmaxf(x, __shfl_xor(x, 32, 64));
+}
+
+struct WaveState {
+  v4f acc[8];     // O^T tiles: lane l holds head l%16, channels 16ct + 4(l/16) + r
+  float m;        // running max (log2 domain), the same on the 4 lanes of a head
+  float l;        // this lane's share of the weight sum
+};
+
+// Online-softmax update with the 16 logits (log2 domain) of this lane;
+// returns the weights as f16 relative to 2^(m - lfm) (lfm = log2 of the
+// V-scale mantissa folded into them).
+__device__ __forceinline__ void rescale(WaveState& st, const float (&y)[16]) {
+  float bm = y[0];
+#pragma unroll
+  for (int i = 1; i < 16; ++i) bm = fmaxf(bm, y[i]);
+  bm = xgroup_max(bm);
+  const float mnew = bm > st.m + kLazyD ? bm : st.m;
+  if (__ballot(mnew != st.m)) {
+    const float corr = __builtin_amdgcn_exp2f(st.m - mnew);
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct) st.acc[ct] *= corr;
+    st.l *= corr;
+    st.m = mnew;
+  }
+}
+
+template <int BITS, int FMT>
+__device__ __forceinline__ void process_block(WaveState& st, const QRegs<BITS>& r,
+                                              const v8h (&qh)[4], float cs, float sv_rel,
+                                              int n_valid, int G) {
+  // S^T = K q^T: 4 tiles of 16 keys, 4 steps of 32 channels
+  v4f sc[4];
+  const I4Scale k4 = make_i4scale(1.0f);
+  const VScale k8 = make_vscale(1.0f);
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    sc[t] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      v8h ka;
+      if constexpr (BITS == 4) ka = i4x8_to_h_perm(r.k[t][0][s], k4);
+      else ka = b8x8_to_h<FMT>(r.k[t][s >> 1][(s & 1) * 2], r.k[t][s >> 1][(s & 1) * 2 + 1], k8);
+      sc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka, qh[s], sc[t], 0, 0, 0);
+    }
+  }
+  float y[16];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) y[t * 4 + q] = sc[t][q] * cs;
+  if (n_valid < kBlock) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (G * 16 + t * 4 + q >= n_valid) y[t * 4 + q] = -INFINITY;
+  }
+  rescale(st, y);
+  // V scale relative to the wave's reference: fm * 2^ev, fm in [1/2, 1)
+  int ev = 0;
+  float fm = 1.0f;
+  if (sv_rel > 0.0f) fm = __builtin_frexpf(sv_rel, &ev);
+  const float mb = st.m - __builtin_amdgcn_logf(fm);
+  _Float16 p[16];
+  float ps = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    p[i] = (_Float16)__builtin_amdgcn_exp2f(y[i] - mb);
+    ps += (float)p[i];
+  }
+  st.l += ps * __builtin_amdgcn_rcpf(fm);
+  const bool tiny = ev < -24;   // 2^ev below the f16 range: the block adds nothing
+  const float p2 = tiny ? 0.0f : __builtin_ldexpf(1.0f, ev);
+  const I4Scale v4 = make_i4scale(p2);
+  VScale v8 = make_vscale(p2);
+  // O^T += V^T P^T: 8 channel tiles x 2 steps of 32 keys
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    v8h pb;
+    if constexpr (BITS == 4) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        pb[2 * q] = p[(2 * s) * 4 + q];
+        pb[2 * q + 1] = p[(2 * s + 1) * 4 + q];
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        pb[q] = p[(2 * s) * 4 + q];
+        pb[4 + q] = p[(2 * s + 1) * 4 + q];
+      }
+    }
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct) {
+      v8h va;
+      if constexpr (BITS == 4) va = i4x8_to_h_perm(r.v[ct][s], v4);
+      else va = b8x8_to_h<FMT>(r.v[ct][2 * s], r.v[ct][2 * s + 1], v8);
+      st.acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb, st.acc[ct], 0, 0, 0);
+    }
+  }
+}
+
+// One tile of 64 full-precision rows (vertical lines or ring slots).
+__device__ __forceinline__ void process_fp_tile(WaveState& st, const DecodeArgs& a, int bj,
+                                                int tile, const v8bf (&qb)[4], int hl, int G) {
+  const int base = tile * kBlock;
+  v4u kr[4][4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const v4u* p = reinterpret_cast<const v4u*>(
+        a.fk + ((size_t)bj * a.nfp + base + unit_row(t, hl)) * kHeadDim + G * 32);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) kr[t][s] = __builtin_nontemporal_load(p + s);
+  }
+  v4f sc[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    sc[t] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      sc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, kr[t][s]), qb[s],
+                                                      sc[t], 0, 0, 0);
+  }
+  v4u vr[8][2];
+#pragma unroll
+  for (int ct = 0; ct < 8; ++ct) {
+    const v4u* p = reinterpret_cast<const v4u*>(
+        a.fv + ((size_t)bj * kHeadDim + ct * 16 + hl) * a.nfp + base + G * 16);
+    vr[ct][0] = __builtin_nontemporal_load(p);
+    vr[ct][1] = __builtin_nontemporal_load(p + 1);
+  }
+  float y[16];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int i = base + G * 16 + t * 4 + q;
+      int rs = i - a.vl_rows - a.ring_head;
+      if (rs < 0) rs += a.ring_rows;
+      const bool valid = i < a.n_vl || (i >= a.vl_rows && rs < a.ring_valid);
+      y[t * 4 + q] = valid ? sc[t][q] * a.c_log2 : -INFINITY;
+    }
+  rescale(st, y);
+  uint32_t hi[16], lo[16];
+  float ps = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const float pv = __builtin_amdgcn_exp2f(y[i] - st.m);
+    const uint32_t hb = __float_as_uint(pv) & 0xffff0000u;
+    const float rem = pv - __uint_as_float(hb);
+    const uint32_t lb = __float_as_uint(rem);
+    const uint32_t lr = (lb + 0x7fffu + ((lb >> 16) & 1u)) & 0xffff0000u;   // round to nearest even
+    hi[i] = hb >> 16;
+    lo[i] = lr >> 16;
+    ps += __uint_as_float(hb) + __uint_as_float(lr);
+  }
+  st.l += ps;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    v4u ph, pl;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      ph[q] = hi[(2 * s) * 4 + 2 * q] | (hi[(2 * s) * 4 + 2 * q + 1] << 16);
+      ph[2 + q] = hi[(2 * s + 1) * 4 + 2 * q] | (hi[(2 * s + 1) * 4 + 2 * q + 1] << 16);
+      pl[q] = lo[(2 * s) * 4 + 2 * q] | (lo[(2 * s) * 4 + 2 * q + 1] << 16);
+      pl[2 + q] = lo[(2 * s + 1) * 4 + 2 * q] | (lo[(2 * s + 1) * 4 + 2 * q + 1] << 16);
+    }
+    const v8bf bh = __builtin_bit_cast(v8bf, ph), bl = __builtin_bit_cast(v8bf, pl);
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct) {
+      const v8bf va = __builtin_bit_cast(v8bf, vr[ct][s]);
+      st.acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, bh, st.acc[ct], 0, 0, 0);
+      st.acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, bl, st.acc[ct], 0, 0, 0);
+    }
+  }
+}
+
+template <int BITS, int FMT>
+__global__ void __launch_bounds__(kDecThreads, 2)
+decode_attn_kernel(DecodeArgs a) {
+  __shared__ float r_acc[kDecWaves][kMaxGroup][kHeadDim];
+  __shared__ float r_m[kDecWaves][kMaxGroup], r_l[kDecWaves][kMaxGroup];
+  const int bj = blockIdx.y, split = blockIdx.x;
+  const int b = bj / a.Hkv, j = bj - b * a.Hkv;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int hl = lane & 15, G = lane >> 4;
+
+  // query operands: lane (head hl, group G) holds channels 32G .. 32G+31
+  v4u qw[4];
+  if (hl < a.g) {
+    const v4u* p = reinterpret_cast<const v4u*>(
+        a.q + ((size_t)b * a.Hq + (size_t)j * a.g + hl) * kHeadDim + G * 32);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) qw[s] = p[s];
+  } else {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) qw[s] = v4u{0u, 0u, 0u, 0u};
+  }
+
+  WaveState st;
+#pragma unroll
+  for (int ct = 0; ct < 8; ++ct) st.acc[ct] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+  st.m = kMinusBigD;
+  st.l = 0.0f;
+  float vref = 1.0f;
+
+  if (split < a.S_q) {
+    // f16 query: q * 2^eq with max |q * 2^eq| in [2^14, 2^15) per head
+    uint32_t mx = 0;
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        mx = max(mx, qw[s][e] & 0x7fffu);
+        mx = max(mx, (qw[s][e] >> 16) & 0x7fffu);
+      }
+    float qmax = bf16_bits_to_f32(mx);
+    qmax = xgroup_max(qmax);
+    int E = 0;
+    if (qmax > 0.0f) frexpf(qmax, &E);
+    const int eq = qmax > 0.0f ? 15 - E : 0;
+    const float qmul = __builtin_ldexpf(1.0f, eq);
+    v8h qh[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      float f[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        f[2 * e] = bf16_lo(qw[s][e]) * qmul;
+        f[2 * e + 1] = bf16_hi(qw[s][e]) * qmul;
+      }
+      if constexpr (BITS == 4) {
+        const int ord[8] = {0, 4, 1, 5, 2, 6, 3, 7};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qh[s][e] = (_Float16)f[ord[e]];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qh[s][e] = (_Float16)f[e];
+      }
+    }
+    const float c_q = a.c_log2 * __builtin_ldexpf(1.0f, -eq);
+
+    // blocks of this wave: first + 4i, i < U
+    const int first = split * kDecWaves * a.U + w;
+    const size_t sbase = (size_t)bj * a.cap_blocks;
+    float vmax = 0.0f;
+    for (int i = 0; i < a.U; ++i) {
+      const int blk = first + kDecWaves * i;
+      if (blk < a.nbq) vmax = fmaxf(vmax, a.vs[sbase + blk]);
+    }
+    int Ev = 0;
+    if (vmax > 0.0f) frexpf(vmax, &Ev);
+    vref = __builtin_ldexpf(1.0f, Ev);
+    const float inv_vref = __builtin_ldexpf(1.0f, -Ev);
+
+    QRegs<BITS> cur, nxt;
+    if (first < a.nbq) load_block<BITS>(cur, a, bj, first, hl, G);
+    for (int i = 0; i < a.U; ++i) {
+      const int blk = first + kDecWaves * i;
+      if (blk >= a.nbq) break;
+      const int nblk = blk + kDecWaves;
+      const bool more = i + 1 < a.U && nblk < a.nbq;
+      if (more) load_block<BITS>(nxt, a, bj, nblk, hl, G);
+      const float sk = a.ks[sbase + blk], sv = a.vs[sbase + blk];
+      const int n_valid = blk == a.nbf - 1 ? a.n_last : kBlock;
+      process_block<BITS, FMT>(st, cur, qh, c_q * sk, sv * inv_vref, n_valid, G);
+      if (more) cur = nxt;
+    }
+  } else {
+    const int tile = (split - a.S_q) * kDecWaves + w;
+    if (tile < a.nfp / kBlock) {
+      v8bf qb[4];
+#pragma unroll
+      for (int s = 0; s < 4; ++s) qb[s] = __builtin_bit_cast(v8bf, qw[s]);
+      process_fp_tile(st, a, bj, tile, qb, hl, G);
+    }
+  }
+
+  // wave totals -> LDS
+  float l = st.l;
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  if (hl < a.g) {
+    if (G == 0) {
+      r_m[w][hl] = st.m;
+      r_l[w][hl] = l;
+    }
+#pragma unroll
+    for (int ct = 0; ct < 8; ++ct)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) r_acc[w][hl][ct * 16 + G * 4 + q] = st.acc[ct][q] * vref;
+  }
+  __syncthreads();
+  // merge the 4 waves: one partial per query head of the group
+  const int S = a.S_q + a.S_f;
+  for (int e = threadIdx.x; e < a.g * kHeadDim; e += kDecThreads) {
+    const int h = e >> 7, c = e & (kHeadDim - 1);
+    float M = r_m[0][h];
+#pragma unroll
+    for (int v = 1; v < kDecWaves; ++v) M = fmaxf(M, r_m[v][h]);
+    float acc = 0.0f, lsum = 0.0f;
+#pragma unroll
+    for (int v = 0; v < kDecWaves; ++v) {
+      const float f = __builtin_amdgcn_exp2f(r_m[v][h] - M);
+      acc += r_acc[v][h][c] * f;
+      lsum += r_l[v][h] * f;
+    }
+    float* dst = a.part + (((size_t)bj * S + split) * a.g + h) * kPartStride;
+    dst[c] = acc;
+    if (c == 0) {
+      dst[kHeadDim] = M;
+      dst[kHeadDim + 1] = lsum;
+    }
+  }
+}
+
+// ReduceSoftmax over the S partials of each (b, h): one workgroup per query
+// row, one thread per channel.
+__global__ void __launch_bounds__(kHeadDim)
+decode_combine_kernel(const float* __restrict__ part, void* __restrict__ out, int Hq, int Hkv,
+                      int g, int S, int out_bf16) {
+  const int bh = blockIdx.x;
+  const int b = bh / Hq, h = bh - b * Hq;
+  const int j = h / g, r = h - j * g;
+  const size_t bj = (size_t)b * Hkv + j;
+  const int c = threadIdx.x;
+  float M = kMinusBigD;
+  for (int s = 0; s < S; ++s) M = fmaxf(M, part[((bj * S + s) * g + r) * kPartStride + kHeadDim]);
+  float acc = 0.0f, l = 0.0f;
+  for (int s = 0; s < S; ++s) {
+    const float* p = part + ((bj * S + s) * g + r) * kPartStride;
+    const float f = __builtin_amdgcn_exp2f(p[kHeadDim] - M);
+    acc += p[c] * f;
+    l += p[kHeadDim + 1] * f;
+  }
+  const float o = acc / l;
+  if (out_bf16) {
+    const uint32_t u = __float_as_uint(o);
+    reinterpret_cast<uint16_t*>(out)[(size_t)bh * kHeadDim + c] =
+        (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+  } else {
+    reinterpret_cast<float*>(out)[(size_t)bh * kHeadDim + c] = o;
+  }
+}
+
+}  // namespace
+
+// ---- host launchers -------------------------------------------------------
+
+DecodeSplit decode_split(const hyq_dcache& c) {
+  DecodeSplit d;
+  const int nbf = (c.n_frozen + kBlock - 1) / kBlock;
+  d.nbq = nbf + c.n_merged;
+  const int64_t total = (int64_t)c.B * c.Hkv * d.nbq;
+  int64_t U = (total + 4095) / 4096;
+  if (U < 2) U = 2;
+  if (U > 64) U = 64;
+  d.U = (int)U;
+  d.S_q = (d.nbq + kDecWaves * d.U - 1) / (kDecWaves * d.U);
+  const int nft = (c.vl_rows + c.ring_rows) / kBlock;
+  d.S_f = (nft + kDecWaves - 1) / kDecWaves;
+  return d;
+}
+
+size_t decode_ws_bytes(const hyq_dcache& c) {
+  const int nft = (c.vl_rows + c.ring_rows) / kBlock;
+  const int64_t S = (c.cap_blocks + 2 * kDecWaves - 1) / (2 * kDecWaves) +
+                    (nft + kDecWaves - 1) / kDecWaves;
+  return (size_t)c.B * c.Hkv * S * (c.Hq / c.Hkv) * kPartStride * sizeof(float);
+}
+
+hipError_t launch_freeze_gather(const hyq_dcache& c, int N, const uint16_t* K, const uint16_t* V,
+                                hipStream_t st) {
+  const int nfp = c.vl_rows + c.ring_rows;
+  dim3 grid(nfp / kBlock, c.B * c.Hkv);
+  freeze_gather_kernel<<<grid, 256, 0, st>>>(K, V, c.vl_pos, static_cast<uint16_t*>(c.fp_k),
+                                             static_cast<uint16_t*>(c.fp_v), N, c.window, c.n_vl,
+                                             c.vl_rows, nfp);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_append(const hyq_dcache& c, const uint16_t* k_new, const uint16_t* v_new,
+                                bool merge, int slot, hipStream_t st) {
+  AppendArgs a;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.fk = static_cast<uint16_t*>(c.fp_k);
+  a.fv = static_cast<uint16_t*>(c.fp_v);
+  a.kc = static_cast<uint8_t*>(c.k_codes);
+  a.vc = static_cast<uint8_t*>(c.v_codes);
+  a.ks = c.k_scale;
+  a.vs = c.v_scale;
+  a.q_pos = c.q_pos;
+  a.nfp = c.vl_rows + c.ring_rows;
+  a.vl_rows = c.vl_rows;
+  a.ring_rows = c.ring_rows;
+  a.W = c.window;
+  a.merge = merge ? 1 : 0;
+  a.head = c.ring_head;
+  a.blk = (c.n_frozen + kBlock - 1) / kBlock + c.n_merged;
+  a.cap_blocks = c.cap_blocks;
+  a.pos0 = (int)(c.t - c.n_staged - c.window);
+  a.slot = slot;
+  dim3 grid(c.B * c.Hkv, 2);
+  if (c.kv_format == HYQ_FMT_FP8) append_kernel<8, HYQ_FMT_FP8><<<grid, kQuantThreads, 0, st>>>(a);
+  else if (c.bits_kv == 8) append_kernel<8, HYQ_FMT_INT><<<grid, kQuantThreads, 0, st>>>(a);
+  else append_kernel<4, HYQ_FMT_INT><<<grid, kQuantThreads, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_attn(const hyq_dcache& c, const uint16_t* q, float softmax_scale,
+                              void* out, int out_dtype, float* part, hipStream_t st) {
+  const DecodeSplit d = decode_split(c);
+  DecodeArgs a;
+  a.kc = static_cast<const uint8_t*>(c.k_codes);
+  a.vc = static_cast<const uint8_t*>(c.v_codes);
+  a.ks = c.k_scale;
+  a.vs = c.v_scale;
+  a.fk = static_cast<const uint16_t*>(c.fp_k);
+  a.fv = static_cast<const uint16_t*>(c.fp_v);
+  a.q = q;
+  a.part = part;
+  a.Hq = c.Hq;
+  a.Hkv = c.Hkv;
+  a.g = c.Hq / c.Hkv;
+  a.cap_blocks = c.cap_blocks;
+  a.nbq = d.nbq;
+  a.nbf = (c.n_frozen + kBlock - 1) / kBlock;
+  a.n_last = c.n_frozen - (a.nbf - 1) * kBlock;
+  a.n_vl = c.n_vl;
+  a.vl_rows = c.vl_rows;
+  a.nfp = c.vl_rows + c.ring_rows;
+  a.ring_head = c.ring_head;
+  a.ring_rows = c.ring_rows;
+  a.ring_valid = c.window + c.n_staged;
+  a.S_q = d.S_q;
+  a.S_f = d.S_f;
+  a.U = d.U;
+  a.c_log2 = softmax_scale * 1.4426950408889634f;
+  const int S = d.S_q + d.S_f;
+  dim3 grid(S, c.B * c.Hkv);
+  if (c.kv_format == HYQ_FMT_FP8)
+    decode_attn_kernel<8, HYQ_FMT_FP8><<<grid, kDecThreads, 0, st>>>(a);
+  else if (c.bits_kv == 8)
+    decode_attn_kernel<8, HYQ_FMT_INT><<<grid, kDecThreads, 0, st>>>(a);
+  else
+    decode_attn_kernel<4, HYQ_FMT_INT><<<grid, kDecThreads, 0, st>>>(a);
+  decode_combine_kernel<<<c.B * c.Hq, kHeadDim, 0, st>>>(part, out, c.Hq, c.Hkv, a.g, S,
+                                                         out_dtype);
+  return hipGetLastError();
+}
+
+}  // namespace hyq

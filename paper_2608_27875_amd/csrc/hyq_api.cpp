@@ -94,6 +94,88 @@ int check_shape(const hyq_shape* s, hyq_sizes* z) {
   return HYQ_OK;
 }
 
+int64_t round_up64(int64_t x) { return (x + 63) / 64 * 64; }
+
+// Geometry of the decode cache of a prefill shape (Algorithm 4's buffers);
+// state zeroed, pointers NULL.
+int dcache_geometry(const hyq_shape* s, int64_t max_tokens, hyq_dcache* c, hyq_dcache_sizes* out) {
+  hyq_sizes z;
+  int rc = check_shape(s, &z);
+  if (rc) return rc;
+  if (s->bits_kv == 16)
+    return fail(HYQ_EINVAL, "the decode cache needs a quantized format (bits_kv 8 or 4)");
+  if (s->window < HYQ_DECODE_WS)
+    return fail(HYQ_EINVAL, "decode needs window >= %d (the staging buffer merges %d window "
+                "tokens at a time), got %d", HYQ_DECODE_WS, HYQ_DECODE_WS, s->window);
+  if (s->L < s->window)
+    return fail(HYQ_EINVAL, "decode needs a prefill of at least window tokens (L = %d < W = %d)",
+                s->L, s->window);
+  if (max_tokens < s->L || max_tokens > (int64_t)0x7fffffff)
+    return fail(HYQ_EINVAL, "max_tokens must be in [L, 2^31 - 1] (got %lld)",
+                (long long)max_tokens);
+  memset(c, 0, sizeof *c);
+  c->B = s->B;
+  c->Hq = s->Hq;
+  c->Hkv = s->Hkv;
+  c->D = s->D;
+  c->window = s->window;
+  c->bits_kv = s->bits_kv;
+  c->kv_format = s->kv_format;
+  c->n_vl = z.k;
+  c->vl_rows = (int32_t)round_up64(z.k);
+  c->ring_rows = (int32_t)(round_up64(s->window) + HYQ_DECODE_WS);
+  c->n_frozen = z.nQ;
+  const int64_t nbf = (z.nQ + 63) / 64;
+  const int64_t merges = (max_tokens - s->L + HYQ_DECODE_WS - 1) / HYQ_DECODE_WS;
+  if (nbf + merges > (int64_t)1 << 24) return fail(HYQ_EUNSUPPORTED, "cache too long");
+  c->cap_blocks = (int32_t)(nbf + merges);
+  c->t = s->L;
+  if (out) {
+    const size_t BH = (size_t)s->B * s->Hkv, D = s->D, cap = c->cap_blocks;
+    const size_t row = s->bits_kv == 8 ? D : D / 2;
+    const size_t nfp = (size_t)c->vl_rows + c->ring_rows;
+    memset(out, 0, sizeof *out);
+    out->k_codes_bytes = BH * cap * 64 * row;
+    out->v_codes_bytes = BH * cap * D * (64 * s->bits_kv / 8);
+    out->k_scale_bytes = out->v_scale_bytes = BH * cap * 4;
+    out->q_pos_bytes = BH * cap * 64 * 4;
+    out->fp_k_bytes = out->fp_v_bytes = BH * nfp * D * 2;
+    out->vl_pos_bytes = BH * (size_t)z.k * 4;
+    out->freeze_ws_bytes = z.select_ws_bytes;
+    out->attn_ws_bytes = hyq::decode_ws_bytes(*c);
+  }
+  return HYQ_OK;
+}
+
+// Consistency of a cache struct (geometry as dcache_geometry makes it, state
+// in range, buffers present).
+int check_dcache(const hyq_dcache* c) {
+  if (!c) return fail(HYQ_EINVAL, "cache is NULL");
+  if (c->B < 1 || c->Hq < 1 || c->Hkv < 1 || c->Hq % c->Hkv || c->Hq / c->Hkv > 8 ||
+      c->D != hyq::kHeadDim)
+    return fail(HYQ_EINVAL, "cache geometry is invalid (B, Hq, Hkv, D)");
+  if ((c->bits_kv != 8 && c->bits_kv != 4) ||
+      (c->kv_format != HYQ_FMT_INT && c->kv_format != HYQ_FMT_FP8) ||
+      (c->kv_format == HYQ_FMT_FP8 && c->bits_kv != 8))
+    return fail(HYQ_EINVAL, "cache format is invalid (bits_kv %d, kv_format %d)", c->bits_kv,
+                c->kv_format);
+  if (c->window < HYQ_DECODE_WS || c->n_vl < 0 || c->vl_rows != round_up64(c->n_vl) ||
+      c->ring_rows != round_up64(c->window) + HYQ_DECODE_WS || c->n_frozen < 0)
+    return fail(HYQ_EINVAL, "cache geometry is invalid (window, n_vl, vl_rows, ring_rows)");
+  const int64_t nbf = (c->n_frozen + 63) / 64;
+  if (c->n_merged < 0 || nbf + c->n_merged > c->cap_blocks || c->n_staged < 0 ||
+      c->n_staged > HYQ_DECODE_WS || c->ring_head < 0 || c->ring_head >= c->ring_rows ||
+      c->ring_head % 64 != 0 || c->t < (int64_t)c->window)
+    return fail(HYQ_EINVAL, "cache state is invalid (n_merged %d, n_staged %d, ring_head %d)",
+                c->n_merged, c->n_staged, c->ring_head);
+  if (!c->fp_k || !c->fp_v) return fail(HYQ_EINVAL, "fp_k and fp_v must be non-NULL");
+  if (c->cap_blocks > 0 &&
+      (!c->k_codes || !c->v_codes || !c->k_scale || !c->v_scale || !c->q_pos))
+    return fail(HYQ_EINVAL, "k_codes, v_codes, k_scale, v_scale and q_pos must be non-NULL");
+  if (c->n_vl > 0 && !c->vl_pos) return fail(HYQ_EINVAL, "vl_pos must be non-NULL when n_vl > 0");
+  return HYQ_OK;
+}
+
 int hip_status(hipError_t e, const char* what) {
   if (e != hipSuccess) return fail(HYQ_EHIP, "%s: %s", what, hipGetErrorString(e));
   return ok();
@@ -194,6 +276,112 @@ HYQ_API int hyq_attn_prefill(const hyq_shape* shape, const void* Q, const void* 
           static_cast<const uint8_t*>(k_codes), k_scale, static_cast<const uint8_t*>(v_codes),
           v_scale, kq_pos, softmax_scale, out, out_dtype, static_cast<hipStream_t>(stream)),
       "hyq_attn_prefill launch");
+}
+
+HYQ_API int hyq_dcache_init(const hyq_shape* prefill, int64_t max_tokens, hyq_dcache* cache,
+                            hyq_dcache_sizes* sizes) {
+  if (!cache) return fail(HYQ_EINVAL, "cache is NULL");
+  hyq_dcache c;
+  hyq_dcache_sizes z;
+  const int rc = dcache_geometry(prefill, max_tokens, &c, &z);
+  if (rc) return rc;
+  *cache = c;
+  if (sizes) *sizes = z;
+  return ok();
+}
+
+HYQ_API int hyq_freeze(const hyq_shape* prefill, const void* Q, const void* K, const void* V,
+                       hyq_dcache* cache, void* ws, size_t ws_bytes, void* stream) {
+  hyq_sizes z;
+  int rc = check_shape(prefill, &z);
+  if (rc) return rc;
+  rc = check_dcache(cache);
+  if (rc) return rc;
+  if (!Q || !K || !V) return fail(HYQ_EINVAL, "Q, K and V must be non-NULL");
+  hyq_dcache ref;
+  hyq_dcache_sizes rz;
+  rc = dcache_geometry(prefill, prefill->L, &ref, &rz);
+  if (rc) return rc;
+  if (ref.B != cache->B || ref.Hq != cache->Hq || ref.Hkv != cache->Hkv ||
+      ref.window != cache->window || ref.bits_kv != cache->bits_kv ||
+      ref.kv_format != cache->kv_format || ref.n_vl != cache->n_vl ||
+      ref.n_frozen != cache->n_frozen || cache->cap_blocks < (ref.n_frozen + 63) / 64)
+    return fail(HYQ_EINVAL, "cache geometry does not match the prefill shape");
+  if (rz.freeze_ws_bytes > 0 && (!ws || ws_bytes < rz.freeze_ws_bytes))
+    return fail(HYQ_EINVAL, "workspace too small: %zu bytes given, %zu needed", ws_bytes,
+                rz.freeze_ws_bytes);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int BHkv = prefill->B * prefill->Hkv;
+  if (z.k > 0) {
+    float* qsum = static_cast<float*>(ws);
+    float* sc = reinterpret_cast<float*>(static_cast<char*>(ws) +
+                                         align256((size_t)BHkv * prefill->D * 4));
+    hipError_t e = hyq::launch_select(*prefill, z, static_cast<const uint16_t*>(Q),
+                                      static_cast<const uint16_t*>(K), cache->vl_pos, sc, qsum, st);
+    if (e != hipSuccess) return hip_status(e, "hyq_freeze selection launch");
+  }
+  if (cache->cap_blocks > 0) {
+    hyq::launch_compact(cache->vl_pos, cache->q_pos, z.k, z.P, z.nQ, cache->cap_blocks * 64,
+                        BHkv, st);
+    hyq::launch_quant_kv(prefill->bits_kv, prefill->kv_format, static_cast<const uint16_t*>(K),
+                         static_cast<const uint16_t*>(V), cache->q_pos,
+                         static_cast<uint8_t*>(cache->k_codes), cache->k_scale,
+                         static_cast<uint8_t*>(cache->v_codes), cache->v_scale, prefill->L, z.nQ,
+                         z.n_kvblk, cache->cap_blocks, BHkv, st);
+  }
+  const hipError_t e = hyq::launch_freeze_gather(*cache, prefill->L,
+                                                 static_cast<const uint16_t*>(K),
+                                                 static_cast<const uint16_t*>(V), st);
+  if (e != hipSuccess) return hip_status(e, "hyq_freeze launch");
+  cache->n_merged = 0;
+  cache->ring_head = 0;
+  cache->n_staged = 0;
+  cache->t = prefill->L;
+  return ok();
+}
+
+HYQ_API int hyq_decode_append(hyq_dcache* cache, const void* k_new, const void* v_new,
+                              void* stream) {
+  const int rc = check_dcache(cache);
+  if (rc) return rc;
+  if (!k_new || !v_new) return fail(HYQ_EINVAL, "k_new and v_new must be non-NULL");
+  const bool merge = cache->n_staged == HYQ_DECODE_WS;
+  const int nbf = (cache->n_frozen + 63) / 64;
+  if (merge && nbf + cache->n_merged >= cache->cap_blocks)
+    return fail(HYQ_EINVAL, "decode cache full: all %d quantized blocks are in use",
+                cache->cap_blocks);
+  if (cache->t >= (int64_t)0x7fffffff) return fail(HYQ_EINVAL, "decode cache full (positions)");
+  const int head = merge ? (cache->ring_head + HYQ_DECODE_WS) % cache->ring_rows : cache->ring_head;
+  const int staged = merge ? 0 : cache->n_staged;
+  const int slot = (head + cache->window + staged) % cache->ring_rows;
+  const hipError_t e = hyq::launch_decode_append(*cache, static_cast<const uint16_t*>(k_new),
+                                                 static_cast<const uint16_t*>(v_new), merge, slot,
+                                                 static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_status(e, "hyq_decode_append launch");
+  if (merge) cache->n_merged += 1;
+  cache->ring_head = head;
+  cache->n_staged = staged + 1;
+  cache->t += 1;
+  return ok();
+}
+
+HYQ_API int hyq_decode_attn(const hyq_dcache* cache, const void* q, float softmax_scale,
+                            void* out, int32_t out_dtype, void* ws, size_t ws_bytes,
+                            void* stream) {
+  const int rc = check_dcache(cache);
+  if (rc) return rc;
+  if (!q || !out) return fail(HYQ_EINVAL, "q and out must be non-NULL");
+  if (out_dtype != 0 && out_dtype != 1)
+    return fail(HYQ_EINVAL, "out_dtype must be 0 (float32) or 1 (bf16), got %d", out_dtype);
+  if (!(softmax_scale > 0.0f) || softmax_scale == INFINITY)
+    return fail(HYQ_EINVAL, "softmax_scale must be positive and finite");
+  const size_t need = hyq::decode_ws_bytes(*cache);
+  if (!ws || ws_bytes < need)
+    return fail(HYQ_EINVAL, "workspace too small: %zu bytes given, %zu needed", ws_bytes, need);
+  return hip_status(hyq::launch_decode_attn(*cache, static_cast<const uint16_t*>(q), softmax_scale,
+                                            out, out_dtype, static_cast<float*>(ws),
+                                            static_cast<hipStream_t>(stream)),
+                    "hyq_decode_attn launch");
 }
 
 }  // extern "C"

@@ -29,6 +29,31 @@ hipError_t launch_attn_prefill(const hyq_shape& s, const hyq_sizes& z, const uin
                                const int32_t* kq_pos, float softmax_scale, void* out,
                                int out_dtype, hipStream_t st);
 
+// Building blocks of hyq_quantize, reused by the decode cache's Freeze:
+// compaction of the non-vertical prefix into kq_pos (nslots slots per (b, j))
+// and the K/V block quantization of n_blocks blocks, each (b, j) owning
+// blk_stride blocks of the outputs.
+void launch_compact(const int32_t* idx, int32_t* kq_pos, int k, int P, int nQ, int nslots,
+                    int BHkv, hipStream_t st);
+void launch_quant_kv(int bits, int fmt, const uint16_t* K, const uint16_t* V,
+                     const int32_t* kq_pos, uint8_t* k_codes, float* k_scale, uint8_t* v_codes,
+                     float* v_scale, int L, int nQ, int n_blocks, int blk_stride, int BHkv,
+                     hipStream_t st);
+
+// Decode: split of the sequence axis (blocks per wave U, quantized splits
+// S_q, full-precision splits S_f), workspace size, and the launches.
+struct DecodeSplit {
+  int nbq, U, S_q, S_f;
+};
+DecodeSplit decode_split(const hyq_dcache& c);
+size_t decode_ws_bytes(const hyq_dcache& c);
+hipError_t launch_freeze_gather(const hyq_dcache& c, int N, const uint16_t* K, const uint16_t* V,
+                                hipStream_t st);
+hipError_t launch_decode_append(const hyq_dcache& c, const uint16_t* k_new, const uint16_t* v_new,
+                                bool merge, int slot, hipStream_t st);
+hipError_t launch_decode_attn(const hyq_dcache& c, const uint16_t* q, float softmax_scale,
+                              void* out, int out_dtype, float* part, hipStream_t st);
+
 // ---- device helpers -------------------------------------------------------
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) {

@@ -1,0 +1,58 @@
+// Device helpers of per-block symmetric quantization (Algorithm 2, Stage 2),
+// shared by the prefill quantizer and the decode cache's block merges.
+#pragma once
+
+#include "hyq_internal.h"
+
+namespace hyq {
+
+constexpr int kQuantThreads = 256;
+
+// Maximum over the kQuantThreads threads of a workgroup (every thread gets it).
+__device__ __forceinline__ float block_max(float v, float* sh) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) sh[w] = v;
+  __syncthreads();
+  float r = sh[0];
+  for (int i = 1; i < kQuantThreads / 64; ++i) r = fmaxf(r, sh[i]);
+  __syncthreads();
+  return r;
+}
+
+// 32 bf16 values (64 bytes) as float.
+__device__ __forceinline__ void load32(const uint16_t* p, float* x) {
+  const uint4* q = reinterpret_cast<const uint4*>(p);
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const uint4 w = q[u];
+    const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[u * 8 + 2 * e] = bf16_lo(ww[e]);
+      x[u * 8 + 2 * e + 1] = bf16_hi(ww[e]);
+    }
+  }
+}
+
+__device__ __forceinline__ int quant1(float x, float s, float c) {
+  // s > 0 here; x / s is the correctly rounded IEEE quotient
+  const float q = __builtin_rintf(x / s);
+  return (int)fminf(fmaxf(q, -c), c);
+}
+
+// E4M3 bit pattern of x / s (s > 0); the clamp keeps -0 and bounds the
+// quotient by the largest finite value.
+__device__ __forceinline__ int quant1_fp8(float x, float s) {
+  const float y = fminf(fmaxf(x / s, -448.0f), 448.0f);
+  return __builtin_amdgcn_cvt_pk_fp8_f32(y, 0.0f, 0, false) & 0xff;
+}
+
+template <int FMT>
+__device__ __forceinline__ int quant_code(float x, float s, float c) {
+  if (FMT == HYQ_FMT_FP8) return quant1_fp8(x, s);
+  return quant1(x, s, c);
+}
+
+}  // namespace hyq

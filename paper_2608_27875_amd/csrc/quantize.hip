@@ -17,13 +17,13 @@
 // definition bit for bit.  HBM-bound: each input row is read once and each
 // code written once, with 16-byte accesses.
 #include "hyq_internal.h"
+#include "quant_dev.h"
 
 #pragma clang fp contract(off)
 
 namespace hyq {
 namespace {
 
-constexpr int kQuantThreads = 256;
 constexpr int kMaxLdsIdx = 8192;
 
 // slots n < nQ: the n-th non-vertical prefix position; slots [nQ, nslots):
@@ -52,52 +52,6 @@ compact_kernel(const int32_t* __restrict__ idx, int32_t* __restrict__ kq_pos, in
     if (!vertical && slot >= 0 && slot < nQ) out[slot] = i;
   }
   if (i >= nQ && i < nslots) out[i] = HYQ_KQ_POS_PAD;
-}
-
-__device__ __forceinline__ float block_max(float v, float* sh) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  const int w = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) sh[w] = v;
-  __syncthreads();
-  float r = sh[0];
-  for (int i = 1; i < kQuantThreads / 64; ++i) r = fmaxf(r, sh[i]);
-  __syncthreads();
-  return r;
-}
-
-// 32 bf16 values (64 bytes) as float.
-__device__ __forceinline__ void load32(const uint16_t* p, float* x) {
-  const uint4* q = reinterpret_cast<const uint4*>(p);
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const uint4 w = q[u];
-    const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      x[u * 8 + 2 * e] = bf16_lo(ww[e]);
-      x[u * 8 + 2 * e + 1] = bf16_hi(ww[e]);
-    }
-  }
-}
-
-__device__ __forceinline__ int quant1(float x, float s, float c) {
-  // s > 0 here; x / s is the correctly rounded IEEE quotient
-  const float q = __builtin_rintf(x / s);
-  return (int)fminf(fmaxf(q, -c), c);
-}
-
-// E4M3 bit pattern of x / s (s > 0); the clamp keeps -0 and bounds the
-// quotient by the largest finite value.
-__device__ __forceinline__ int quant1_fp8(float x, float s) {
-  const float y = fminf(fmaxf(x / s, -448.0f), 448.0f);
-  return __builtin_amdgcn_cvt_pk_fp8_f32(y, 0.0f, 0, false) & 0xff;
-}
-
-template <int FMT>
-__device__ __forceinline__ int quant_code(float x, float s, float c) {
-  if (FMT == HYQ_FMT_FP8) return quant1_fp8(x, s);
-  return quant1(x, s, c);
 }
 
 // Thread layout of one 64 x 128 block: row = tid / 4, channels (tid % 4) * 32 .. +32.
@@ -142,6 +96,8 @@ quant_q_kernel(const uint16_t* __restrict__ Q, int8_t* __restrict__ qc, float* _
 
 // One workgroup per (b, j, compacted block).  K codes are written row-major,
 // V codes channel-major (the block transposed) through an LDS tile.
+// n_kvblk is the number of blocks each (b, j) owns in the outputs (kq_pos
+// slots n_kvblk * 64); the grid may cover fewer.
 template <int BITS, int FMT>
 __global__ void __launch_bounds__(kQuantThreads)
 quant_kv_kernel(const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
@@ -242,36 +198,45 @@ quant_kv_kernel(const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
 
 }  // namespace
 
+void launch_compact(const int32_t* idx, int32_t* kq_pos, int k, int P, int nQ, int nslots,
+                    int BHkv, hipStream_t st) {
+  const int span = P > nslots ? P : nslots;
+  if (nslots <= 0) return;
+  dim3 cg((span + 255) / 256, BHkv);
+  compact_kernel<<<cg, 256, 0, st>>>(idx, kq_pos, k, P, nQ, nslots);
+}
+
+void launch_quant_kv(int bits, int fmt, const uint16_t* K, const uint16_t* V,
+                     const int32_t* kq_pos, uint8_t* k_codes, float* k_scale, uint8_t* v_codes,
+                     float* v_scale, int L, int nQ, int n_blocks, int blk_stride, int BHkv,
+                     hipStream_t st) {
+  if (n_blocks <= 0) return;
+  dim3 kg(n_blocks, BHkv);
+  if (fmt == HYQ_FMT_FP8)
+    quant_kv_kernel<8, HYQ_FMT_FP8><<<kg, kQuantThreads, 0, st>>>(
+        K, V, kq_pos, k_codes, k_scale, v_codes, v_scale, L, nQ, blk_stride);
+  else if (bits == 8)
+    quant_kv_kernel<8, HYQ_FMT_INT><<<kg, kQuantThreads, 0, st>>>(
+        K, V, kq_pos, k_codes, k_scale, v_codes, v_scale, L, nQ, blk_stride);
+  else
+    quant_kv_kernel<4, HYQ_FMT_INT><<<kg, kQuantThreads, 0, st>>>(
+        K, V, kq_pos, k_codes, k_scale, v_codes, v_scale, L, nQ, blk_stride);
+}
+
 hipError_t launch_quantize(const hyq_shape& s, const hyq_sizes& z, const uint16_t* Q,
                            const uint16_t* K, const uint16_t* V, const int32_t* idx,
                            int8_t* q_codes, float* q_scale, uint8_t* k_codes, float* k_scale,
                            uint8_t* v_codes, float* v_scale, int32_t* kq_pos, hipStream_t st) {
   if (s.bits_kv == 16) return hipSuccess;
   const int BHkv = s.B * s.Hkv;
-  const int nslots = z.n_kvblk * kBlock;
-  const int span = z.P > nslots ? z.P : nslots;
-  if (nslots > 0) {
-    dim3 cg((span + 255) / 256, BHkv);
-    compact_kernel<<<cg, 256, 0, st>>>(idx, kq_pos, z.k, z.P, z.nQ, nslots);
-  }
-  const bool fp8 = s.kv_format == HYQ_FMT_FP8;
+  launch_compact(idx, kq_pos, z.k, z.P, z.nQ, z.n_kvblk * kBlock, BHkv, st);
   dim3 qg(z.n_qblk, s.B * s.Hq);
-  if (fp8)
+  if (s.kv_format == HYQ_FMT_FP8)
     quant_q_kernel<HYQ_FMT_FP8><<<qg, kQuantThreads, 0, st>>>(Q, q_codes, q_scale, s.L, z.n_qblk);
   else
     quant_q_kernel<HYQ_FMT_INT><<<qg, kQuantThreads, 0, st>>>(Q, q_codes, q_scale, s.L, z.n_qblk);
-  if (z.n_kvblk > 0) {
-    dim3 kg(z.n_kvblk, BHkv);
-    if (fp8)
-      quant_kv_kernel<8, HYQ_FMT_FP8><<<kg, kQuantThreads, 0, st>>>(
-          K, V, kq_pos, k_codes, k_scale, v_codes, v_scale, s.L, z.nQ, z.n_kvblk);
-    else if (s.bits_kv == 8)
-      quant_kv_kernel<8, HYQ_FMT_INT><<<kg, kQuantThreads, 0, st>>>(
-          K, V, kq_pos, k_codes, k_scale, v_codes, v_scale, s.L, z.nQ, z.n_kvblk);
-    else
-      quant_kv_kernel<4, HYQ_FMT_INT><<<kg, kQuantThreads, 0, st>>>(
-          K, V, kq_pos, k_codes, k_scale, v_codes, v_scale, s.L, z.nQ, z.n_kvblk);
-  }
+  launch_quant_kv(s.bits_kv, s.kv_format, K, V, kq_pos, k_codes, k_scale, v_codes, v_scale, s.L,
+                  z.nQ, z.n_kvblk, z.n_kvblk, BHkv, st);
   return hipGetLastError();
 }
 

@@ -113,3 +113,111 @@ def test_strerror(lib):
     assert hyq.hyq_strerror(-1) == "invalid argument"
     assert hyq.hyq_strerror(-2) == "unsupported configuration"
     assert hyq.hyq_strerror(-3) == "HIP runtime error"
+
+
+# ---- decode cache (Algorithms 3 and 4) --------------------------------------
+
+def _dshape(**kw):
+    base = dict(B=1, Hq=32, Hkv=8, L=32768, D=128, window=128, budget_ppm=50000, bits_kv=4,
+                block=64)
+    base.update(kw)
+    return hyq.Shape(**base)
+
+
+def test_dcache_struct_layout_matches_header(tmp_path):
+    """sizeof/offsetof of hyq_dcache and hyq_dcache_sizes from the C header
+    (compiled with gcc) against the binding's ctypes structures."""
+    import subprocess
+    fields = hyq._DCACHE_INTS + ("t",) + hyq._DCACHE_PTRS
+    src = ['#include <stdio.h>', '#include <stddef.h>', '#include "hyq.h"', 'int main(void) {',
+           'printf("%zu %zu\\n", sizeof(hyq_dcache), sizeof(hyq_dcache_sizes));']
+    src += [f'printf("%zu\\n", offsetof(hyq_dcache, {f}));' for f in fields]
+    src += [f'printf("%zu\\n", offsetof(hyq_dcache_sizes, {f}));' for f in hyq._DSIZES]
+    src += ['return 0; }']
+    c = tmp_path / "layout.c"
+    c.write_text("\n".join(src))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(c), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split()
+    vals = [int(v) for v in out]
+    assert vals[0] == ctypes.sizeof(hyq._DCache) and vals[1] == ctypes.sizeof(hyq._DCacheSizes)
+    offs = vals[2:2 + len(fields)]
+    assert offs == [getattr(hyq._DCache, f).offset for f in fields]
+    assert vals[2 + len(fields):] == [getattr(hyq._DCacheSizes, f).offset for f in hyq._DSIZES]
+
+
+@pytest.mark.parametrize("L,W,ppm,bits,extra", [
+    (32768, 128, 50000, 4, 1024), (1000, 64, 20000, 8, 0), (517, 100, 20000, 4, 200),
+    (200, 64, 1000000, 4, 64), (64, 64, 50000, 8, 140), (450, 96, 0, 8, 1),
+])
+def test_dcache_geometry(lib, L, W, ppm, bits, extra):
+    s = _dshape(L=L, window=W, budget_ppm=ppm, bits_kv=bits)
+    c, z = hyq.hyq_dcache_init(s, L + extra)
+    o = orc.sizes(L, W, ppm)
+    rup = lambda x: -(-x // 64) * 64
+    assert c.n_vl == o["k"] and c.n_frozen == o["nQ"]
+    assert c.vl_rows == rup(o["k"]) and c.ring_rows == rup(W) + hyq.DECODE_WS
+    assert c.cap_blocks == o["n_kvblk"] + -(-extra // 64)
+    assert (c.n_merged, c.ring_head, c.n_staged, c.t) == (0, 0, 0, L)
+    BH, nfp, cap = 8, c.vl_rows + c.ring_rows, c.cap_blocks
+    assert z["k_codes_bytes"] == BH * cap * 64 * (128 if bits == 8 else 64)
+    assert z["v_codes_bytes"] == BH * cap * 128 * (64 if bits == 8 else 32)
+    assert z["fp_k_bytes"] == z["fp_v_bytes"] == BH * nfp * 128 * 2
+    assert z["q_pos_bytes"] == BH * cap * 64 * 4 and z["vl_pos_bytes"] == BH * o["k"] * 4
+    assert z["freeze_ws_bytes"] == hyq.hyq_sizes_for(s)["select_ws_bytes"]
+    assert z["attn_ws_bytes"] > 0
+
+
+@pytest.mark.parametrize("kw,max_extra", [
+    (dict(window=32), 0), (dict(L=100, window=128), 0), (dict(bits_kv=16), 0),
+    (dict(), -1), (dict(D=64), 0),
+])
+def test_dcache_bad_geometry_rejected(lib, kw, max_extra):
+    s = _dshape(**kw)
+    with pytest.raises(hyq.HyqError):
+        hyq.hyq_dcache_init(s, s.L + max_extra)
+
+
+def test_decode_calls_reject_bad_arguments_before_launch(lib):
+    s = _dshape(L=1000, window=64, budget_ppm=20000, bits_kv=8)
+    c, z = hyq.hyq_dcache_init(s, 1200)
+    fake = 0x1000                      # never dereferenced: validation fails first
+    N = None
+    # buffers missing
+    assert lib.hyq_decode_append(ctypes.byref(c), ctypes.c_void_p(fake), ctypes.c_void_p(fake),
+                                 N) == hyq.HYQ_EINVAL
+    for n in hyq._DCACHE_PTRS:
+        setattr(c, n, fake)
+    f = ctypes.c_void_p(fake)
+    # bad state
+    c.n_staged = 65
+    assert lib.hyq_decode_append(ctypes.byref(c), f, f, N) == hyq.HYQ_EINVAL
+    c.n_staged = 0
+    c.ring_head = 5
+    assert lib.hyq_decode_attn(ctypes.byref(c), f, ctypes.c_float(0.088), f, 0, f,
+                               z["attn_ws_bytes"], N) == hyq.HYQ_EINVAL
+    c.ring_head = 0
+    # full cache: a merge is due and every block is in use
+    c.n_staged = 64
+    c.n_merged = c.cap_blocks - -(-c.n_frozen // 64)
+    assert lib.hyq_decode_append(ctypes.byref(c), f, f, N) == hyq.HYQ_EINVAL
+    assert "full" in hyq.hyq_last_error()
+    assert c.n_staged == 64                        # state unchanged
+    c.n_merged = 0
+    # workspace too small, bad out dtype, bad scale, missing q
+    assert lib.hyq_decode_attn(ctypes.byref(c), f, ctypes.c_float(0.088), f, 0, f,
+                               z["attn_ws_bytes"] - 1, N) == hyq.HYQ_EINVAL
+    assert "workspace" in hyq.hyq_last_error()
+    assert lib.hyq_decode_attn(ctypes.byref(c), f, ctypes.c_float(0.088), f, 2, f,
+                               z["attn_ws_bytes"], N) == hyq.HYQ_EINVAL
+    assert lib.hyq_decode_attn(ctypes.byref(c), f, ctypes.c_float(-1.0), f, 0, f,
+                               z["attn_ws_bytes"], N) == hyq.HYQ_EINVAL
+    assert lib.hyq_decode_attn(ctypes.byref(c), N, ctypes.c_float(0.088), f, 0, f,
+                               z["attn_ws_bytes"], N) == hyq.HYQ_EINVAL
+    # freeze: shape that does not match the cache
+    other = ctypes.byref(_dshape(L=1001, window=64, budget_ppm=20000, bits_kv=8).c())
+    assert lib.hyq_freeze(other, f, f, f, ctypes.byref(c), f, z["freeze_ws_bytes"],
+                          N) == hyq.HYQ_EINVAL
+    assert "match" in hyq.hyq_last_error()
+    assert lib.hyq_freeze(ctypes.byref(s.c()), f, f, f, ctypes.byref(c), f,
+                          z["freeze_ws_bytes"] - 1, N) == hyq.HYQ_EINVAL

@@ -155,3 +155,13 @@ def test_decode_weights_sum_to_one_and_key_order_irrelevant():
     # a value shift by a constant row shifts every output by that row
     c2 = orc.freeze(d["Q"], d["K"], d["V"] * 0, 1, W, 20000, 8)   # all-zero values
     assert np.all(orc.decode_attention(q, c2) == 0)
+
+
+def test_freeze_domain():
+    d = _prefill(10, 1, 2, 1, 100, 8, 64)
+    with pytest.raises(ValueError):
+        orc.freeze(d["Q"], d["K"], d["V"], 1, 32, 10000, 8)        # W < Ws
+    with pytest.raises(ValueError):
+        orc.freeze(d["Q"], d["K"], d["V"], 1, 128, 10000, 8)       # N < W
+    with pytest.raises(ValueError):
+        orc.freeze(d["Q"], d["K"], d["V"], 1, 64, 10000, 16)       # nothing quantized
