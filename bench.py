@@ -7,6 +7,15 @@ resident in HBM.  Default workload: GQA 32 query / 8 KV heads, head dim 128,
 32768 tokens, window 256, vertical budget 1%, 8-bit K/V, float32 output (the
 launch configuration the parity tests check at full size).
 
+The ``decode`` sub-record times the decode path (Algorithm 3 over the
+cache Freeze builds) on the paper's decode-latency workload: batch 1, 32
+query / 8 KV heads, 32k-token prefix, K4V4, top-5% vertical lines, window
+128.  It measures one attention call per layer over 36 layer caches
+(about 1.4 GB, so that the last-level cache cannot serve repeated reads),
+against its roofline, HBM bandwidth.  A second line uses batch 16.  The
+same kernel with every prefix token kept in bf16 is the in-house
+full-precision comparison.
+
 Prints one JSON line.  ``value`` is the algorithmic causal attention FLOPs
 (4 * D * Hq * B * L(L+1)/2) per second of the whole step, in TFLOP/s;
 ``roofline`` describes the attention kernel alone (timed with HIP events on
@@ -102,6 +111,119 @@ def cpu_baseline(d, cfg, flops_total, budget_s):
     }
 
 
+def decode_bytes(c, B):
+    """Algorithmic HBM bytes of one decode attention call: every valid cache
+    entry once (codes, scales, bf16 rows), the query and the output."""
+    Hkv, D = c.Hkv, c.D
+    nbq = -(-c.n_frozen // 64) + c.n_merged
+    nq = c.n_frozen + 64 * c.n_merged
+    row = D if c.bits_kv == 8 else D // 2
+    per_head = 2 * nq * row + 2 * nbq * 4 + (c.n_vl + c.window + c.n_staged) * D * 2 * 2
+    return B * Hkv * per_head + B * c.Hq * D * (2 + 4)
+
+
+def decode_record(B, layers, steps, budget_ppm=50000, bits=4, N=32768, W=128, Hq=32, Hkv=8,
+                  seed=0, label=None):
+    """Freeze `layers` synthetic layers, then time hyq_decode_attn over all of
+    them (one decode token of a `layers`-layer model)."""
+    import numpy as np
+    import torch
+
+    import paper_2608_27875_amd as hyq
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    shape = hyq.Shape(B=B, Hq=Hq, Hkv=Hkv, L=N, window=W, budget_ppm=budget_ppm, bits_kv=bits)
+    gen_ = torch.Generator(device=dev)
+    gen_.manual_seed(seed)
+    caches, qs, outs = [], [], []
+    print(f"[bench] decode: freezing {layers} layers of {shape}", file=sys.stderr, flush=True)
+    for _ in range(layers):
+        Q = torch.randn((B, Hq, N, 128), generator=gen_, device=dev).to(torch.bfloat16)
+        K = torch.randn((B, Hkv, N, 128), generator=gen_, device=dev).to(torch.bfloat16)
+        V = torch.randn((B, Hkv, N, 128), generator=gen_, device=dev).to(torch.bfloat16)
+        c = hyq.DecodeCache(shape, N + 64, dev)
+        hyq.hyq_freeze(shape, Q, K, V, c, stream)
+        del Q, K, V
+        caches.append(c)
+        qs.append(torch.randn((B, Hq, 128), generator=gen_, device=dev).to(torch.bfloat16))
+        outs.append(torch.empty((B, Hq, 128), dtype=torch.float32, device=dev))
+    torch.cuda.synchronize()
+
+    def one_token():
+        for c, q, o in zip(caches, qs, outs):
+            hyq.hyq_decode_attn(c, q, o)   # on the current stream (the capture stream below)
+
+    def timed(run):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(steps)]
+        s = torch.cuda.current_stream()
+        for e in ev:
+            e[0].record(s)
+            run()
+            e[1].record(s)
+        torch.cuda.synchronize()
+        return float(np.median([e[0].elapsed_time(e[1]) for e in ev]))
+
+    for _ in range(3):
+        one_token()
+    torch.cuda.synchronize()
+    ref = [o.clone() for o in outs]
+    ms_eager = timed(one_token)
+    # the same launches replayed as one HIP graph (no host work between
+    # kernels); every replay must reproduce the eager outputs bit for bit
+    graph_ok, ms = False, ms_eager
+    try:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            one_token()
+        torch.cuda.synchronize()
+        graph_ok = True
+        for _ in range(3):
+            for o in outs:
+                o.zero_()
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            graph_ok &= all(torch.equal(o, r) for o, r in zip(outs, ref))
+        if graph_ok:
+            ms = timed(g.replay)
+        del g
+    except RuntimeError as e:
+        print(f"[bench] decode graph capture failed: {e}", file=sys.stderr, flush=True)
+    us_layer = ms * 1e3 / layers
+    nbytes = decode_bytes(caches[0].c, B)
+    gbs = nbytes / (us_layer * 1e-6) / 1e9
+    rec = {"workload": label or (f"decode_gqa{Hq}q{Hkv}kv_d128_B{B}_N{N}_W{W}_r{budget_ppm}ppm_"
+                                 f"kv{bits}bit"),
+           "layers": layers, "us_per_layer": round(us_layer, 3),
+           "timing": "hip graph of the layer loop" if graph_ok else "eager launches",
+           "us_per_layer_eager": round(ms_eager * 1e3 / layers, 3),
+           "ms_per_token_all_layers": round(ms, 4),
+           "bytes_per_layer": int(nbytes),
+           "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                        "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                        "kernel": "decode_attn_kernel + decode_combine_kernel"}}
+    del caches, qs, outs
+    torch.cuda.empty_cache()
+    return rec
+
+
+def decode_section(layers, steps):
+    """The decode measurements: K4V4 hybrid at batch 1 and 16, and the
+    all-bf16 comparison (every prefix token a vertical line) at batch 1."""
+    r1 = decode_record(1, layers, steps)
+    bf = decode_record(1, layers, steps, budget_ppm=1000000, bits=8,
+                       label="decode_gqa32q8kv_d128_B1_N32768_all_bf16")
+    r1["bf16_same_length"] = {"us_per_layer": bf["us_per_layer"],
+                              "bytes_per_layer": bf["bytes_per_layer"],
+                              "achieved_gbs": bf["roofline"]["achieved"],
+                              "speedup_of_hybrid": round(bf["us_per_layer"] / r1["us_per_layer"], 3)}
+    r16 = decode_record(16, max(2, layers // 9), steps)
+    r1["batch16"] = {k: r16[k] for k in ("workload", "layers", "us_per_layer", "bytes_per_layer",
+                                         "roofline")}
+    return r1
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -123,6 +245,10 @@ def main():
                     help="code format of the quantized path (fp8 = OCP E4M3, 8-bit only)")
     ap.add_argument("--no-fp8", action="store_true",
                     help="skip the FP8-code run of the same inputs")
+    ap.add_argument("--no-decode", action="store_true", help="skip the decode measurement")
+    ap.add_argument("--decode-only", action="store_true",
+                    help="only the decode measurement (printed as its own JSON line)")
+    ap.add_argument("--decode-layers", type=int, default=36)
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for rocprofv3 --pmc runs: one step, a plain 1 GiB copy kernel of known "
                          "traffic (the counter scale), one more step; no timing")
@@ -139,6 +265,10 @@ def main():
 
     import paper_2608_27875_amd as hyq
     from paper_2608_27875_amd import gen
+
+    if args.decode_only:
+        print(json.dumps({"decode": decode_section(args.decode_layers, args.steps)}), flush=True)
+        return
 
     cfg = dict(gen.CONFIGS[args.config])
     if args.bits is not None:
@@ -344,6 +474,8 @@ def main():
         "quantize_gbs": round(q_bytes / (np.mean(qnt) * 1e-3) / 1e9, 1) if q_bytes else None,
         "planted_recall": round(float(np.mean(recall)), 4) if recall else None,
     }
+    rec["decode"] = None if args.no_decode else decode_section(args.decode_layers,
+                                                                 min(args.steps, 20))
     if not args.no_cpu_baseline:
         print(f"[bench] cpu baseline (oracle, ~{args.cpu_budget_s:.0f} s)", file=sys.stderr,
               flush=True)

@@ -41,7 +41,7 @@ typedef unsigned v2u __attribute__((ext_vector_type(2)));
 
 constexpr int kDecWaves = 4;
 constexpr int kDecThreads = kDecWaves * 64;
-constexpr int kPartStride = 132;           // floats per partial: acc[128], m, l, pad
+constexpr int kPartStride = kDecodePartFloats;
 constexpr float kLazyD = 8.0f;             // rescale only when the max grows by > 2^8
 constexpr float kMinusBigD = -1.0e30f;
 constexpr int kMaxGroup = 8;
@@ -231,8 +231,6 @@ append_kernel(AppendArgs a) {
 struct DecodeArgs {
   const uint8_t* kc;
   const uint8_t* vc;
-  const float* ks;
-  const float* vs;
   const uint16_t* fk;
   const uint16_t* fv;
   const uint16_t* q;
@@ -251,7 +249,9 @@ struct DecodeArgs {
 // code * 2^e in the element order [0, 4, 1, 5, 2, 6, 3, 7]: each nibble,
 // biased by 8, is placed in the low mantissa bits of 1024 (f16 0x6400),
 // either at bit 0 (value 1024 + u) or at bit 4 (1024 + 16 u), and one fused
-// multiply-add per pair removes the offset and applies 2^e.  Exact.
+// multiply-add per pair removes the offset and applies 2^e.  Exact.  The
+// bias is folded into the constants: ((w ^ 0x88888888) & M) | 0x6400_6400 =
+// (w & M) ^ D with D = (0x88888888 & M) | 0x64006400, one 3-input logic op.
 struct I4Scale {
   v2h m1, b1, m16, b16;
 };
@@ -266,12 +266,13 @@ __device__ __forceinline__ I4Scale make_i4scale(float p2) {
   return s;
 }
 __device__ __forceinline__ v8h i4x8_to_h_perm(uint32_t w, const I4Scale& s) {
-  const uint32_t u = w ^ 0x88888888u;
-  const uint32_t u8 = u >> 8;
-  const v2h a = __builtin_bit_cast(v2h, (u & 0x000F000Fu) | 0x64006400u);
-  const v2h b = __builtin_bit_cast(v2h, (u & 0x00F000F0u) | 0x64006400u);
-  const v2h c = __builtin_bit_cast(v2h, (u8 & 0x000F000Fu) | 0x64006400u);
-  const v2h d = __builtin_bit_cast(v2h, (u8 & 0x00F000F0u) | 0x64006400u);
+  constexpr uint32_t M0 = 0x000F000Fu, D0 = 0x64086408u;   // nibbles 0, 4 (after >> 8: 2, 6)
+  constexpr uint32_t M1 = 0x00F000F0u, D1 = 0x64806480u;   // nibbles 1, 5 (after >> 8: 3, 7)
+  const uint32_t w8 = w >> 8;
+  const v2h a = __builtin_bit_cast(v2h, (w & M0) ^ D0);
+  const v2h b = __builtin_bit_cast(v2h, (w & M1) ^ D1);
+  const v2h c = __builtin_bit_cast(v2h, (w8 & M0) ^ D0);
+  const v2h d = __builtin_bit_cast(v2h, (w8 & M1) ^ D1);
   const v2h ha = __builtin_elementwise_fma(a, s.m1, s.b1);    // elements 0, 4
   const v2h hb = __builtin_elementwise_fma(b, s.m16, s.b16);  // elements 1, 5
   const v2h hc = __builtin_elementwise_fma(c, s.m1, s.b1);    // elements 2, 6
@@ -288,32 +289,40 @@ __device__ __forceinline__ v8h b8x8_to_h(uint32_t w0, uint32_t w1, const VScale&
   return __builtin_bit_cast(v8h, v4u{h[0], h[1], h[2], h[3]});
 }
 
-// Per-block code registers of one wave: K rows of the 4 MFMA tiles, V^T rows
-// of the 8 channel tiles.
+// Per-block registers of one wave: K rows of the 4 MFMA tiles, V^T rows of
+// the 8 channel tiles, and the block's two scales.
 template <int BITS>
 struct QRegs {
   static constexpr int kK = BITS == 8 ? 2 : 1;   // 16-byte loads per K tile
   v4u k[4][kK];
   typename std::conditional<BITS == 8, v4u, v2u>::type v[8];
+  float sk, sv;
 };
 
 // Row of the unit read by MFMA tile t, A-operand row m: (m/4)*16 + 4t + m%4,
 // so that accumulator register r of lane l holds key (l/16)*16 + 4t + r.
 __device__ __forceinline__ int unit_row(int t, int m) { return ((m >> 2) << 4) + (t << 2) + (m & 3); }
 
+// blk is wave-uniform, so the two scale loads are scalar loads, which complete
+// independently of the vector loads of the codes.
 template <int BITS>
-__device__ __forceinline__ void load_block(QRegs<BITS>& r, const DecodeArgs& a, int bj, int blk,
+__device__ __forceinline__ void load_block(QRegs<BITS>& r, const DecodeArgs& a,
+                                           const float* __restrict__ ks,
+                                           const float* __restrict__ vs, int bj, int blk,
                                            int hl, int G) {
   constexpr int kRow = BITS == 8 ? kHeadDim : kHeadDim / 2;
   constexpr int vRow = BITS == 8 ? kBlock : kBlock / 2;
-  const uint8_t* kb = a.kc + ((size_t)bj * a.cap_blocks + blk) * kBlock * kRow;
+  const size_t cb = (size_t)bj * a.cap_blocks + blk;
+  r.sk = ks[cb];
+  r.sv = vs[cb];
+  const uint8_t* kb = a.kc + cb * kBlock * kRow;
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     const v4u* p = reinterpret_cast<const v4u*>(kb + unit_row(t, hl) * kRow + G * (kRow / 4));
 #pragma unroll
     for (int u = 0; u < QRegs<BITS>::kK; ++u) r.k[t][u] = __builtin_nontemporal_load(p + u);
   }
-  const uint8_t* vb = a.vc + ((size_t)bj * a.cap_blocks + blk) * kHeadDim * vRow;
+  const uint8_t* vb = a.vc + cb * kHeadDim * vRow;
 #pragma unroll
   for (int ct = 0; ct < 8; ++ct) {
     const uint8_t* p = vb + (ct * 16 + hl) * vRow + G * (vRow / 4);
@@ -327,79 +336,91 @@ __device__ __forceinline__ float xgroup_max(float x) {
   return fmaxf(x, __shfl_xor(x, 32, 64));
 }
 
+// Online state of one wave.  The accumulator holds sum p * value / 2^eref,
+// eref the largest V-scale exponent met so far (blocks with smaller scales
+// enter through smaller weights), so that every f16 weight stays <= 2^8.
 struct WaveState {
   v4f acc[8];     // O^T tiles: lane l holds head l%16, channels 16ct + 4(l/16) + r
   float m;        // running max (log2 domain), the same on the 4 lanes of a head
   float l;        // this lane's share of the weight sum
+  int eref;       // wave-uniform
 };
 
-// Online-softmax update with the 16 logits (log2 domain) of this lane;
-// returns the weights as f16 relative to 2^(m - lfm) (lfm = log2 of the
-// V-scale mantissa folded into them).
-__device__ __forceinline__ void rescale(WaveState& st, const float (&y)[16]) {
-  float bm = y[0];
+// Raise the running max (lazily) and the V-scale exponent to cover a new
+// unit with logits y * cs (cs > 0) and exponent e; rescales the state when
+// either moves.
+__device__ __forceinline__ void advance(WaveState& st, const float (&y)[16], float cs, int e) {
+  float bm = fmaxf(fmaxf(y[0], y[1]), y[2]);
 #pragma unroll
-  for (int i = 1; i < 16; ++i) bm = fmaxf(bm, y[i]);
-  bm = xgroup_max(bm);
+  for (int i = 3; i < 16; i += 2) bm = fmaxf(fmaxf(bm, y[i]), y[i + 1 < 16 ? i + 1 : i]);
+  bm = xgroup_max(bm) * cs;
   const float mnew = bm > st.m + kLazyD ? bm : st.m;
-  if (__ballot(mnew != st.m)) {
-    const float corr = __builtin_amdgcn_exp2f(st.m - mnew);
+  const int enew = e > st.eref ? e : st.eref;
+  if (__ballot(mnew != st.m) || enew != st.eref) {
+    const float cl = __builtin_amdgcn_exp2f(st.m - mnew);
+    const float ca = __builtin_ldexpf(cl, st.eref - enew);
 #pragma unroll
-    for (int ct = 0; ct < 8; ++ct) st.acc[ct] *= corr;
-    st.l *= corr;
+    for (int ct = 0; ct < 8; ++ct) st.acc[ct] *= ca;
+    st.l *= cl;
     st.m = mnew;
+    st.eref = enew;
   }
 }
 
 template <int BITS, int FMT>
 __device__ __forceinline__ void process_block(WaveState& st, const QRegs<BITS>& r,
-                                              const v8h (&qh)[4], float cs, float sv_rel,
-                                              int n_valid, int G) {
+                                              const v8h (&qh)[4], float c_q, int n_valid,
+                                              int G) {
   // S^T = K q^T: 4 tiles of 16 keys, 4 steps of 32 channels
   v4f sc[4];
-  const I4Scale k4 = make_i4scale(1.0f);
-  const VScale k8 = make_vscale(1.0f);
+  const I4Scale one4 = make_i4scale(1.0f);
+  const VScale one8 = make_vscale(1.0f);
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     sc[t] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       v8h ka;
-      if constexpr (BITS == 4) ka = i4x8_to_h_perm(r.k[t][0][s], k4);
-      else ka = b8x8_to_h<FMT>(r.k[t][s >> 1][(s & 1) * 2], r.k[t][s >> 1][(s & 1) * 2 + 1], k8);
+      if constexpr (BITS == 4) ka = i4x8_to_h_perm(r.k[t][0][s], one4);
+      else ka = b8x8_to_h<FMT>(r.k[t][s >> 1][(s & 1) * 2], r.k[t][s >> 1][(s & 1) * 2 + 1], one8);
       sc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka, qh[s], sc[t], 0, 0, 0);
     }
+  }
+  // logits in the log2 domain are sc * cs (cs > 0: a zero K block only has
+  // zero raw scores, so flooring cs changes nothing that matters)
+  const float cs = fmaxf(c_q * r.sk, 1e-30f);
+  if (n_valid < kBlock) {
+    // the ragged last block of the Freeze: padding keys take no weight (a
+    // real branch, not if-converted, since only one block per head has it)
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (G * 16 + t * 4 + q >= n_valid) sc[t][q] = -INFINITY;
   }
   float y[16];
 #pragma unroll
   for (int t = 0; t < 4; ++t)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) y[t * 4 + q] = sc[t][q] * cs;
-  if (n_valid < kBlock) {
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (G * 16 + t * 4 + q >= n_valid) y[t * 4 + q] = -INFINITY;
-  }
-  rescale(st, y);
-  // V scale relative to the wave's reference: fm * 2^ev, fm in [1/2, 1)
-  int ev = 0;
+    for (int q = 0; q < 4; ++q) y[t * 4 + q] = sc[t][q];
+  // V scale sV = fm * 2^e, fm in [1/2, 1); an all-zero block (sV = 0) adds nothing
+  int e = st.eref;
   float fm = 1.0f;
-  if (sv_rel > 0.0f) fm = __builtin_frexpf(sv_rel, &ev);
-  const float mb = st.m - __builtin_amdgcn_logf(fm);
+  if (r.sv > 0.0f) fm = __builtin_frexpf(r.sv, &e);
+  advance(st, y, cs, e);
+  // weights p * fm * 2^(e - eref) in f16 (below 2^-60 they are zero in f16 anyway)
+  const int d = max(e - st.eref, -60);
+  const float nbias = __builtin_amdgcn_logf(fm) + (float)d - st.m;
   _Float16 p[16];
   float ps = 0.0f;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    p[i] = (_Float16)__builtin_amdgcn_exp2f(y[i] - mb);
-    ps += (float)p[i];
+    const float pw = __builtin_amdgcn_exp2f(__builtin_fmaf(y[i], cs, nbias));
+    p[i] = (_Float16)pw;
+    ps += pw;
   }
-  st.l += ps * __builtin_amdgcn_rcpf(fm);
-  const bool tiny = ev < -24;   // 2^ev below the f16 range: the block adds nothing
-  const float p2 = tiny ? 0.0f : __builtin_ldexpf(1.0f, ev);
-  const I4Scale v4 = make_i4scale(p2);
-  VScale v8 = make_vscale(p2);
+  st.l += ps * __builtin_ldexpf(__builtin_amdgcn_rcpf(fm), -d);
   // O^T += V^T P^T: 8 channel tiles x 2 steps of 32 keys
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
@@ -420,14 +441,15 @@ __device__ __forceinline__ void process_block(WaveState& st, const QRegs<BITS>& 
 #pragma unroll
     for (int ct = 0; ct < 8; ++ct) {
       v8h va;
-      if constexpr (BITS == 4) va = i4x8_to_h_perm(r.v[ct][s], v4);
-      else va = b8x8_to_h<FMT>(r.v[ct][2 * s], r.v[ct][2 * s + 1], v8);
+      if constexpr (BITS == 4) va = i4x8_to_h_perm(r.v[ct][s], one4);
+      else va = b8x8_to_h<FMT>(r.v[ct][2 * s], r.v[ct][2 * s + 1], one8);
       st.acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb, st.acc[ct], 0, 0, 0);
     }
   }
 }
 
-// One tile of 64 full-precision rows (vertical lines or ring slots).
+// One tile of 64 full-precision rows (vertical lines or ring slots); their
+// values are exact bf16, a "scale" of 2^0.
 __device__ __forceinline__ void process_fp_tile(WaveState& st, const DecodeArgs& a, int bj,
                                                 int tile, const v8bf (&qb)[4], int hl, int G) {
   const int base = tile * kBlock;
@@ -439,6 +461,14 @@ __device__ __forceinline__ void process_fp_tile(WaveState& st, const DecodeArgs&
 #pragma unroll
     for (int s = 0; s < 4; ++s) kr[t][s] = __builtin_nontemporal_load(p + s);
   }
+  v4u vr[8][2];
+#pragma unroll
+  for (int ct = 0; ct < 8; ++ct) {
+    const v4u* p = reinterpret_cast<const v4u*>(
+        a.fv + ((size_t)bj * kHeadDim + ct * 16 + hl) * a.nfp + base + G * 16);
+    vr[ct][0] = __builtin_nontemporal_load(p);
+    vr[ct][1] = __builtin_nontemporal_load(p + 1);
+  }
   v4f sc[4];
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
@@ -448,40 +478,34 @@ __device__ __forceinline__ void process_fp_tile(WaveState& st, const DecodeArgs&
       sc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, kr[t][s]), qb[s],
                                                       sc[t], 0, 0, 0);
   }
-  v4u vr[8][2];
-#pragma unroll
-  for (int ct = 0; ct < 8; ++ct) {
-    const v4u* p = reinterpret_cast<const v4u*>(
-        a.fv + ((size_t)bj * kHeadDim + ct * 16 + hl) * a.nfp + base + G * 16);
-    vr[ct][0] = __builtin_nontemporal_load(p);
-    vr[ct][1] = __builtin_nontemporal_load(p + 1);
-  }
   float y[16];
 #pragma unroll
   for (int t = 0; t < 4; ++t)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int i = base + G * 16 + t * 4 + q;
-      int rs = i - a.vl_rows - a.ring_head;
-      if (rs < 0) rs += a.ring_rows;
-      const bool valid = i < a.n_vl || (i >= a.vl_rows && rs < a.ring_valid);
-      y[t * 4 + q] = valid ? sc[t][q] * a.c_log2 : -INFINITY;
+      const int r0 = i - a.vl_rows - a.ring_head;
+      const int rs = r0 + (r0 < 0 ? a.ring_rows : 0);
+      const bool valid = (i < a.n_vl) | ((i >= a.vl_rows) & (rs < a.ring_valid));
+      y[t * 4 + q] = valid ? sc[t][q] : -INFINITY;
     }
-  rescale(st, y);
+  advance(st, y, a.c_log2, 0);
+  const int d = max(-st.eref, -60);
+  const float nbias = (float)d - st.m;
   uint32_t hi[16], lo[16];
   float ps = 0.0f;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    const float pv = __builtin_amdgcn_exp2f(y[i] - st.m);
+    const float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(y[i], a.c_log2, nbias));
     const uint32_t hb = __float_as_uint(pv) & 0xffff0000u;
     const float rem = pv - __uint_as_float(hb);
     const uint32_t lb = __float_as_uint(rem);
     const uint32_t lr = (lb + 0x7fffu + ((lb >> 16) & 1u)) & 0xffff0000u;   // round to nearest even
     hi[i] = hb >> 16;
     lo[i] = lr >> 16;
-    ps += __uint_as_float(hb) + __uint_as_float(lr);
+    ps += pv;
   }
-  st.l += ps;
+  st.l += __builtin_ldexpf(ps, -d);
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
     v4u ph, pl;
@@ -502,14 +526,19 @@ __device__ __forceinline__ void process_fp_tile(WaveState& st, const DecodeArgs&
   }
 }
 
+// Grid (S_q + S_f, B*Hkv): workgroups x < S_q take 4U consecutive quantized
+// blocks of KV head (b, j) (wave w: blocks w, w+4, ...), the others 4
+// full-precision tiles (one per wave).  Each workgroup writes one partial
+// (acc[128], m, l) per query head of the group.
 template <int BITS, int FMT>
 __global__ void __launch_bounds__(kDecThreads, 2)
-decode_attn_kernel(DecodeArgs a) {
+decode_attn_kernel(DecodeArgs a, const float* __restrict__ ks, const float* __restrict__ vs) {
   __shared__ float r_acc[kDecWaves][kMaxGroup][kHeadDim];
   __shared__ float r_m[kDecWaves][kMaxGroup], r_l[kDecWaves][kMaxGroup];
   const int bj = blockIdx.y, split = blockIdx.x;
   const int b = bj / a.Hkv, j = bj - b * a.Hkv;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   const int hl = lane & 15, G = lane >> 4;
 
   // query operands: lane (head hl, group G) holds channels 32G .. 32G+31
@@ -529,9 +558,13 @@ decode_attn_kernel(DecodeArgs a) {
   for (int ct = 0; ct < 8; ++ct) st.acc[ct] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
   st.m = kMinusBigD;
   st.l = 0.0f;
-  float vref = 1.0f;
+  st.eref = -1000;
 
   if (split < a.S_q) {
+    const int first = split * kDecWaves * a.U + w;
+    const int n_my = first < a.nbq ? min(a.U, (a.nbq - first + kDecWaves - 1) / kDecWaves) : 0;
+    QRegs<BITS> r0, r1;
+    if (n_my > 0) load_block<BITS>(r0, a, ks, vs, bj, first, hl, G);
     // f16 query: q * 2^eq with max |q * 2^eq| in [2^14, 2^15) per head
     uint32_t mx = 0;
 #pragma unroll
@@ -567,31 +600,32 @@ decode_attn_kernel(DecodeArgs a) {
     }
     const float c_q = a.c_log2 * __builtin_ldexpf(1.0f, -eq);
 
-    // blocks of this wave: first + 4i, i < U
-    const int first = split * kDecWaves * a.U + w;
-    const size_t sbase = (size_t)bj * a.cap_blocks;
-    float vmax = 0.0f;
-    for (int i = 0; i < a.U; ++i) {
+    // two register sets alternate so that the next block's loads are always
+    // in flight while one block is computed; inside the loop every load is
+    // unconditional, which keeps each wait for a block's codes from also
+    // waiting for the prefetched block
+    auto proc = [&](const QRegs<BITS>& r, int i) {
       const int blk = first + kDecWaves * i;
-      if (blk < a.nbq) vmax = fmaxf(vmax, a.vs[sbase + blk]);
-    }
-    int Ev = 0;
-    if (vmax > 0.0f) frexpf(vmax, &Ev);
-    vref = __builtin_ldexpf(1.0f, Ev);
-    const float inv_vref = __builtin_ldexpf(1.0f, -Ev);
-
-    QRegs<BITS> cur, nxt;
-    if (first < a.nbq) load_block<BITS>(cur, a, bj, first, hl, G);
-    for (int i = 0; i < a.U; ++i) {
-      const int blk = first + kDecWaves * i;
-      if (blk >= a.nbq) break;
-      const int nblk = blk + kDecWaves;
-      const bool more = i + 1 < a.U && nblk < a.nbq;
-      if (more) load_block<BITS>(nxt, a, bj, nblk, hl, G);
-      const float sk = a.ks[sbase + blk], sv = a.vs[sbase + blk];
       const int n_valid = blk == a.nbf - 1 ? a.n_last : kBlock;
-      process_block<BITS, FMT>(st, cur, qh, c_q * sk, sv * inv_vref, n_valid, G);
-      if (more) cur = nxt;
+      // keep the scheduler from starting the next block's conversions (and
+      // so waiting for its loads) inside this one
+      __builtin_amdgcn_sched_barrier(0);
+      process_block<BITS, FMT>(st, r, qh, c_q, n_valid, G);
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    int i = 0;
+    for (; i + 2 < n_my; i += 2) {
+      load_block<BITS>(r1, a, ks, vs, bj, first + kDecWaves * (i + 1), hl, G);
+      proc(r0, i);
+      load_block<BITS>(r0, a, ks, vs, bj, first + kDecWaves * (i + 2), hl, G);
+      proc(r1, i + 1);
+    }
+    if (i + 1 < n_my) {
+      load_block<BITS>(r1, a, ks, vs, bj, first + kDecWaves * (i + 1), hl, G);
+      proc(r0, i);
+      proc(r1, i + 1);
+    } else if (i < n_my) {
+      proc(r0, i);
     }
   } else {
     const int tile = (split - a.S_q) * kDecWaves + w;
@@ -603,7 +637,7 @@ decode_attn_kernel(DecodeArgs a) {
     }
   }
 
-  // wave totals -> LDS
+  // wave totals -> LDS (the accumulator back in value units)
   float l = st.l;
   l += __shfl_xor(l, 16, 64);
   l += __shfl_xor(l, 32, 64);
@@ -615,7 +649,8 @@ decode_attn_kernel(DecodeArgs a) {
 #pragma unroll
     for (int ct = 0; ct < 8; ++ct)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) r_acc[w][hl][ct * 16 + G * 4 + q] = st.acc[ct][q] * vref;
+      for (int q = 0; q < 4; ++q)
+        r_acc[w][hl][ct * 16 + G * 4 + q] = __builtin_ldexpf(st.acc[ct][q], st.eref);
   }
   __syncthreads();
   // merge the 4 waves: one partial per query head of the group
@@ -642,23 +677,50 @@ decode_attn_kernel(DecodeArgs a) {
 }
 
 // ReduceSoftmax over the S partials of each (b, h): one workgroup per query
-// row, one thread per channel.
-__global__ void __launch_bounds__(kHeadDim)
+// row; 4 groups of 128 threads (one per channel) each take every 4th
+// partial, with unrolled independent loads, then the groups are merged.
+constexpr int kCombThreads = 512;
+__global__ void __launch_bounds__(kCombThreads)
 decode_combine_kernel(const float* __restrict__ part, void* __restrict__ out, int Hq, int Hkv,
                       int g, int S, int out_bf16) {
+  __shared__ float red[kCombThreads / 64];
+  __shared__ float gacc[kCombThreads / kHeadDim][kHeadDim];
+  __shared__ float gl[kCombThreads / kHeadDim];
   const int bh = blockIdx.x;
   const int b = bh / Hq, h = bh - b * Hq;
   const int j = h / g, r = h - j * g;
   const size_t bj = (size_t)b * Hkv + j;
-  const int c = threadIdx.x;
+  const float* base = part + (bj * S * g + r) * kPartStride;
+  const size_t stride = (size_t)g * kPartStride;
   float M = kMinusBigD;
-  for (int s = 0; s < S; ++s) M = fmaxf(M, part[((bj * S + s) * g + r) * kPartStride + kHeadDim]);
+  for (int s = threadIdx.x; s < S; s += kCombThreads) M = fmaxf(M, base[s * stride + kHeadDim]);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = M;
+  __syncthreads();
+  M = red[0];
+#pragma unroll
+  for (int i = 1; i < kCombThreads / 64; ++i) M = fmaxf(M, red[i]);
+  const int grp = threadIdx.x >> 7, c = threadIdx.x & (kHeadDim - 1);
+  constexpr int kGroups = kCombThreads / kHeadDim;
   float acc = 0.0f, l = 0.0f;
-  for (int s = 0; s < S; ++s) {
-    const float* p = part + ((bj * S + s) * g + r) * kPartStride;
+#pragma unroll 8
+  for (int s = grp; s < S; s += kGroups) {
+    const float* p = base + s * stride;
     const float f = __builtin_amdgcn_exp2f(p[kHeadDim] - M);
     acc += p[c] * f;
     l += p[kHeadDim + 1] * f;
+  }
+  gacc[grp][c] = acc;
+  if (c == 0) gl[grp] = l;
+  __syncthreads();
+  if (grp != 0) return;
+  acc = gacc[0][c];
+  l = gl[0];
+#pragma unroll
+  for (int i = 1; i < kGroups; ++i) {
+    acc += gacc[i][c];
+    l += gl[i];
   }
   const float o = acc / l;
   if (out_bf16) {
@@ -678,11 +740,8 @@ DecodeSplit decode_split(const hyq_dcache& c) {
   DecodeSplit d;
   const int nbf = (c.n_frozen + kBlock - 1) / kBlock;
   d.nbq = nbf + c.n_merged;
-  const int64_t total = (int64_t)c.B * c.Hkv * d.nbq;
-  int64_t U = (total + 4095) / 4096;
-  if (U < 2) U = 2;
-  if (U > 64) U = 64;
-  d.U = (int)U;
+  // about 32 KB of codes per wave, as much as one full-precision tile
+  d.U = c.bits_kv == 4 ? 4 : 2;
   d.S_q = (d.nbq + kDecWaves * d.U - 1) / (kDecWaves * d.U);
   const int nft = (c.vl_rows + c.ring_rows) / kBlock;
   d.S_f = (nft + kDecWaves - 1) / kDecWaves;
@@ -741,8 +800,6 @@ hipError_t launch_decode_attn(const hyq_dcache& c, const uint16_t* q, float soft
   DecodeArgs a;
   a.kc = static_cast<const uint8_t*>(c.k_codes);
   a.vc = static_cast<const uint8_t*>(c.v_codes);
-  a.ks = c.k_scale;
-  a.vs = c.v_scale;
   a.fk = static_cast<const uint16_t*>(c.fp_k);
   a.fv = static_cast<const uint16_t*>(c.fp_v);
   a.q = q;
@@ -767,13 +824,13 @@ hipError_t launch_decode_attn(const hyq_dcache& c, const uint16_t* q, float soft
   const int S = d.S_q + d.S_f;
   dim3 grid(S, c.B * c.Hkv);
   if (c.kv_format == HYQ_FMT_FP8)
-    decode_attn_kernel<8, HYQ_FMT_FP8><<<grid, kDecThreads, 0, st>>>(a);
+    decode_attn_kernel<8, HYQ_FMT_FP8><<<grid, kDecThreads, 0, st>>>(a, c.k_scale, c.v_scale);
   else if (c.bits_kv == 8)
-    decode_attn_kernel<8, HYQ_FMT_INT><<<grid, kDecThreads, 0, st>>>(a);
+    decode_attn_kernel<8, HYQ_FMT_INT><<<grid, kDecThreads, 0, st>>>(a, c.k_scale, c.v_scale);
   else
-    decode_attn_kernel<4, HYQ_FMT_INT><<<grid, kDecThreads, 0, st>>>(a);
-  decode_combine_kernel<<<c.B * c.Hq, kHeadDim, 0, st>>>(part, out, c.Hq, c.Hkv, a.g, S,
-                                                         out_dtype);
+    decode_attn_kernel<4, HYQ_FMT_INT><<<grid, kDecThreads, 0, st>>>(a, c.k_scale, c.v_scale);
+  decode_combine_kernel<<<c.B * c.Hq, kCombThreads, 0, st>>>(part, out, c.Hq, c.Hkv, a.g, S,
+                                                             out_dtype);
   return hipGetLastError();
 }
 

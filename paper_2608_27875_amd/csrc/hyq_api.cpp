@@ -378,6 +378,14 @@ HYQ_API int hyq_decode_attn(const hyq_dcache* cache, const void* q, float softma
   const size_t need = hyq::decode_ws_bytes(*cache);
   if (!ws || ws_bytes < need)
     return fail(HYQ_EINVAL, "workspace too small: %zu bytes given, %zu needed", ws_bytes, need);
+  // the partials this launch writes (never more than `need`; checked so that
+  // a launch can never write past the workspace)
+  const hyq::DecodeSplit d = hyq::decode_split(*cache);
+  const size_t used = (size_t)cache->B * cache->Hkv * (size_t)(d.S_q + d.S_f) *
+                      (cache->Hq / cache->Hkv) * hyq::kDecodePartFloats * sizeof(float);
+  if (used > ws_bytes)
+    return fail(HYQ_EINVAL, "workspace too small for this launch: %zu bytes given, %zu used",
+                ws_bytes, used);
   return hip_status(hyq::launch_decode_attn(*cache, static_cast<const uint16_t*>(q), softmax_scale,
                                             out, out_dtype, static_cast<float*>(ws),
                                             static_cast<hipStream_t>(stream)),

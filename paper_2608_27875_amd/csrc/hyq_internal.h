@@ -45,6 +45,7 @@ void launch_quant_kv(int bits, int fmt, const uint16_t* K, const uint16_t* V,
 struct DecodeSplit {
   int nbq, U, S_q, S_f;
 };
+constexpr int kDecodePartFloats = 132;   // one partial: acc[128], m, l, padding
 DecodeSplit decode_split(const hyq_dcache& c);
 size_t decode_ws_bytes(const hyq_dcache& c);
 hipError_t launch_freeze_gather(const hyq_dcache& c, int N, const uint16_t* K, const uint16_t* V,

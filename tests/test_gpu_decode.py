@@ -219,3 +219,35 @@ def test_decode_32k_k4v4_top5_w128():
         append_both(cache, oc, rng)
     check_attention(cache, oc, rng, label="32k")
     check_cache(cache, oc)
+
+
+def test_decode_attention_in_a_hip_graph():
+    """Decode attention captured in a HIP graph (as a decode loop runs it):
+    each replay, with eager work and synchronizations in between, equals the
+    eager result bit for bit."""
+    import torch
+    shape = hyq.Shape(B=2, Hq=8, Hkv=2, L=800, window=64, budget_ppm=30000, bits_kv=4)
+    d = _inputs("graph", 2, 8, 2, 800, 64)
+    cache, oc = freeze_both(shape, d, 900)
+    rng = np.random.default_rng(8)
+    for _ in range(70):
+        append_both(cache, oc, rng)
+    q = gc.to_dev(_rows(rng, 2, 8))
+    out = torch.empty((2, 8, 128), dtype=torch.float32, device="cuda")
+    hyq.hyq_decode_attn(cache, q, out)
+    torch.cuda.synchronize()
+    ref = out.clone()
+    O = orc.decode_attention(q.view(torch.int16).cpu().numpy().view(np.uint16), oc)
+    mx, mean = gc.attention_error(ref.cpu().numpy(), O)
+    assert mx <= gc.TOL_MAX and mean <= gc.TOL_MEAN
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        hyq.hyq_decode_attn(cache, q, out)
+    for i in range(4):
+        out.fill_(float("nan"))
+        junk = torch.randn(1 << 20, device="cuda").sum()     # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), f"replay {i}"
+        del junk
