@@ -299,9 +299,42 @@ struct QRegs {
   float sk, sv;
 };
 
-// Row of the unit read by MFMA tile t, A-operand row m: (m/4)*16 + 4t + m%4,
-// so that accumulator register r of lane l holds key (l/16)*16 + 4t + r.
+// Row of a quantized block read by MFMA tile t, A-operand row m:
+// (m/4)*16 + 4t + m%4, so that accumulator register r of lane l holds key
+// (l/16)*16 + 4t + r, which is the B-operand order of the P V product.
 __device__ __forceinline__ int unit_row(int t, int m) { return ((m >> 2) << 4) + (t << 2) + (m & 3); }
+
+// Channels of K-step s held by lane group G (8 per step; the k-slice of an
+// MFMA operand may be any set as long as both operands use the same one).
+// Each map makes the 4 lane groups of one load instruction read one
+// contiguous 64-byte run of a row:
+//   kMapI4:   int4 K rows (64 B): channels 32G + 8s .. (one 16-byte load);
+//   kMapB8:   int8 / E4M3 K rows (128 B): load u = s/2 holds channels
+//             64u + 16G .. +16, step s the half s%2 of it;
+//   kMapBF16: bf16 rows (256 B): channels 32s + 8G .. (one load per step).
+constexpr int kMapI4 = 0, kMapB8 = 1, kMapBF16 = 2;
+template <int MAP>
+__device__ __forceinline__ int step_chan(int s, int G) {
+  if constexpr (MAP == kMapI4) return G * 32 + s * 8;
+  else if constexpr (MAP == kMapB8) return (s >> 1) * 64 + G * 16 + (s & 1) * 8;
+  else return s * 32 + G * 8;
+}
+
+// The 4 x 8 query channels of lane (head hl, group G) in the order of a map.
+template <int MAP>
+__device__ __forceinline__ void load_q(v4u (&qw)[4], const uint16_t* qrow, bool ok, int G) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    qw[s] = ok ? *reinterpret_cast<const v4u*>(qrow + step_chan<MAP>(s, G)) : v4u{0u, 0u, 0u, 0u};
+}
+
+// Rows of a full-precision tile read by MFMA tile t, A-operand row m:
+// (t/2)*32 + (m/4)*8 + (t%2)*4 + m%4, so that lane group G holds keys
+// 32s + 8G .. 32s + 8G + 7 for P V step s (tiles 2s, 2s+1), which makes the
+// channel-major V^T loads contiguous too.
+__device__ __forceinline__ int fp_row(int t, int m) {
+  return ((t >> 1) << 5) + ((m >> 2) << 3) + ((t & 1) << 2) + (m & 3);
+}
 
 // blk is wave-uniform, so the two scale loads are scalar loads, which complete
 // independently of the vector loads of the codes.
@@ -318,9 +351,11 @@ __device__ __forceinline__ void load_block(QRegs<BITS>& r, const DecodeArgs& a,
   const uint8_t* kb = a.kc + cb * kBlock * kRow;
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    const v4u* p = reinterpret_cast<const v4u*>(kb + unit_row(t, hl) * kRow + G * (kRow / 4));
+    const uint8_t* row = kb + unit_row(t, hl) * kRow;
 #pragma unroll
-    for (int u = 0; u < QRegs<BITS>::kK; ++u) r.k[t][u] = __builtin_nontemporal_load(p + u);
+    for (int u = 0; u < QRegs<BITS>::kK; ++u)   // channels step_chan(2u, G) .. +16 (8-bit), 32G .. (4-bit)
+      r.k[t][u] = __builtin_nontemporal_load(
+          reinterpret_cast<const v4u*>(row + (BITS == 8 ? u * 64 + G * 16 : G * 16)));
   }
   const uint8_t* vb = a.vc + cb * kHeadDim * vRow;
 #pragma unroll
@@ -456,18 +491,18 @@ __device__ __forceinline__ void process_fp_tile(WaveState& st, const DecodeArgs&
   v4u kr[4][4];
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    const v4u* p = reinterpret_cast<const v4u*>(
-        a.fk + ((size_t)bj * a.nfp + base + unit_row(t, hl)) * kHeadDim + G * 32);
+    const uint16_t* row = a.fk + ((size_t)bj * a.nfp + base + fp_row(t, hl)) * kHeadDim;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) kr[t][s] = __builtin_nontemporal_load(p + s);
+    for (int s = 0; s < 4; ++s)
+      kr[t][s] = __builtin_nontemporal_load(
+          reinterpret_cast<const v4u*>(row + step_chan<kMapBF16>(s, G)));
   }
   v4u vr[8][2];
 #pragma unroll
   for (int ct = 0; ct < 8; ++ct) {
-    const v4u* p = reinterpret_cast<const v4u*>(
-        a.fv + ((size_t)bj * kHeadDim + ct * 16 + hl) * a.nfp + base + G * 16);
-    vr[ct][0] = __builtin_nontemporal_load(p);
-    vr[ct][1] = __builtin_nontemporal_load(p + 1);
+    const uint16_t* vrow = a.fv + ((size_t)bj * kHeadDim + ct * 16 + hl) * a.nfp + base + G * 8;
+    vr[ct][0] = __builtin_nontemporal_load(reinterpret_cast<const v4u*>(vrow));        // keys 8G ..
+    vr[ct][1] = __builtin_nontemporal_load(reinterpret_cast<const v4u*>(vrow + 32));   // keys 32 + 8G ..
   }
   v4f sc[4];
 #pragma unroll
@@ -483,7 +518,7 @@ __device__ __forceinline__ void process_fp_tile(WaveState& st, const DecodeArgs&
   for (int t = 0; t < 4; ++t)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int i = base + G * 16 + t * 4 + q;
+      const int i = base + fp_row(t, G * 4 + q);
       const int r0 = i - a.vl_rows - a.ring_head;
       const int rs = r0 + (r0 < 0 ? a.ring_rows : 0);
       const bool valid = (i < a.n_vl) | ((i >= a.vl_rows) & (rs < a.ring_valid));
@@ -541,17 +576,10 @@ decode_attn_kernel(DecodeArgs a, const float* __restrict__ ks, const float* __re
   const int lane = threadIdx.x & 63;
   const int hl = lane & 15, G = lane >> 4;
 
-  // query operands: lane (head hl, group G) holds channels 32G .. 32G+31
+  // query row of lane (head hl, group G); heads hl >= g are zero columns
+  const bool qok = hl < a.g;
+  const uint16_t* qrow = a.q + ((size_t)b * a.Hq + (size_t)j * a.g + (qok ? hl : 0)) * kHeadDim;
   v4u qw[4];
-  if (hl < a.g) {
-    const v4u* p = reinterpret_cast<const v4u*>(
-        a.q + ((size_t)b * a.Hq + (size_t)j * a.g + hl) * kHeadDim + G * 32);
-#pragma unroll
-    for (int s = 0; s < 4; ++s) qw[s] = p[s];
-  } else {
-#pragma unroll
-    for (int s = 0; s < 4; ++s) qw[s] = v4u{0u, 0u, 0u, 0u};
-  }
 
   WaveState st;
 #pragma unroll
@@ -564,6 +592,7 @@ decode_attn_kernel(DecodeArgs a, const float* __restrict__ ks, const float* __re
     const int first = split * kDecWaves * a.U + w;
     const int n_my = first < a.nbq ? min(a.U, (a.nbq - first + kDecWaves - 1) / kDecWaves) : 0;
     QRegs<BITS> r0, r1;
+    load_q<BITS == 4 ? kMapI4 : kMapB8>(qw, qrow, qok, G);   // first: waits for it never wait for codes
     if (n_my > 0) load_block<BITS>(r0, a, ks, vs, bj, first, hl, G);
     // f16 query: q * 2^eq with max |q * 2^eq| in [2^14, 2^15) per head
     uint32_t mx = 0;
@@ -630,6 +659,7 @@ decode_attn_kernel(DecodeArgs a, const float* __restrict__ ks, const float* __re
   } else {
     const int tile = (split - a.S_q) * kDecWaves + w;
     if (tile < a.nfp / kBlock) {
+      load_q<kMapBF16>(qw, qrow, qok, G);
       v8bf qb[4];
 #pragma unroll
       for (int s = 0; s < 4; ++s) qb[s] = __builtin_bit_cast(v8bf, qw[s]);
@@ -677,58 +707,65 @@ decode_attn_kernel(DecodeArgs a, const float* __restrict__ ks, const float* __re
 }
 
 // ReduceSoftmax over the S partials of each (b, h): one workgroup per query
-// row; 4 groups of 128 threads (one per channel) each take every 4th
-// partial, with unrolled independent loads, then the groups are merged.
+// row.  Thread -> (share ph of the partials, 4 channels): an online max over
+// its share (all loads independent, issued together), then the 16 shares of
+// each channel quad merged through LDS.
 constexpr int kCombThreads = 512;
+constexpr int kCombShares = kCombThreads / (kHeadDim / 4);
 __global__ void __launch_bounds__(kCombThreads)
 decode_combine_kernel(const float* __restrict__ part, void* __restrict__ out, int Hq, int Hkv,
                       int g, int S, int out_bf16) {
-  __shared__ float red[kCombThreads / 64];
-  __shared__ float gacc[kCombThreads / kHeadDim][kHeadDim];
-  __shared__ float gl[kCombThreads / kHeadDim];
+  __shared__ float x_acc[kCombShares][kHeadDim / 4][4];
+  __shared__ float x_m[kCombShares][kHeadDim / 4], x_l[kCombShares][kHeadDim / 4];
   const int bh = blockIdx.x;
   const int b = bh / Hq, h = bh - b * Hq;
   const int j = h / g, r = h - j * g;
   const size_t bj = (size_t)b * Hkv + j;
+  const int c4 = threadIdx.x & 31, ph = threadIdx.x >> 5;
   const float* base = part + (bj * S * g + r) * kPartStride;
   const size_t stride = (size_t)g * kPartStride;
-  float M = kMinusBigD;
-  for (int s = threadIdx.x; s < S; s += kCombThreads) M = fmaxf(M, base[s * stride + kHeadDim]);
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = M;
-  __syncthreads();
-  M = red[0];
-#pragma unroll
-  for (int i = 1; i < kCombThreads / 64; ++i) M = fmaxf(M, red[i]);
-  const int grp = threadIdx.x >> 7, c = threadIdx.x & (kHeadDim - 1);
-  constexpr int kGroups = kCombThreads / kHeadDim;
-  float acc = 0.0f, l = 0.0f;
-#pragma unroll 8
-  for (int s = grp; s < S; s += kGroups) {
+  float M = kMinusBigD, L = 0.0f;
+  v4f acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll 4
+  for (int s = ph; s < S; s += kCombShares) {
     const float* p = base + s * stride;
-    const float f = __builtin_amdgcn_exp2f(p[kHeadDim] - M);
-    acc += p[c] * f;
-    l += p[kHeadDim + 1] * f;
+    const v2u ml = *reinterpret_cast<const v2u*>(p + kHeadDim);
+    const v4f v = *reinterpret_cast<const v4f*>(p + c4 * 4);
+    const float m = __uint_as_float(ml[0]), l = __uint_as_float(ml[1]);
+    const float Mn = fmaxf(M, m);
+    const float a1 = __builtin_amdgcn_exp2f(M - Mn), f = __builtin_amdgcn_exp2f(m - Mn);
+    acc = acc * a1 + v * f;
+    L = L * a1 + l * f;
+    M = Mn;
   }
-  gacc[grp][c] = acc;
-  if (c == 0) gl[grp] = l;
-  __syncthreads();
-  if (grp != 0) return;
-  acc = gacc[0][c];
-  l = gl[0];
+  x_m[ph][c4] = M;
+  x_l[ph][c4] = L;
 #pragma unroll
-  for (int i = 1; i < kGroups; ++i) {
-    acc += gacc[i][c];
-    l += gl[i];
+  for (int e = 0; e < 4; ++e) x_acc[ph][c4][e] = acc[e];
+  __syncthreads();
+  if (ph != 0) return;
+  for (int q = 1; q < kCombShares; ++q) {
+    const float Mn = fmaxf(M, x_m[q][c4]);
+    const float a1 = __builtin_amdgcn_exp2f(M - Mn), f = __builtin_amdgcn_exp2f(x_m[q][c4] - Mn);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] = acc[e] * a1 + x_acc[q][c4][e] * f;
+    L = L * a1 + x_l[q][c4] * f;
+    M = Mn;
   }
-  const float o = acc / l;
+  const float inv = 1.0f / L;
+  const size_t off = (size_t)bh * kHeadDim + c4 * 4;
   if (out_bf16) {
-    const uint32_t u = __float_as_uint(o);
-    reinterpret_cast<uint16_t*>(out)[(size_t)bh * kHeadDim + c] =
-        (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+    uint32_t w[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      uint32_t u0 = __float_as_uint(acc[2 * e] * inv), u1 = __float_as_uint(acc[2 * e + 1] * inv);
+      u0 = (u0 + 0x7fffu + ((u0 >> 16) & 1u)) >> 16;
+      u1 = (u1 + 0x7fffu + ((u1 >> 16) & 1u)) >> 16;
+      w[e] = u0 | (u1 << 16);
+    }
+    *reinterpret_cast<v2u*>(reinterpret_cast<uint16_t*>(out) + off) = v2u{w[0], w[1]};
   } else {
-    reinterpret_cast<float*>(out)[(size_t)bh * kHeadDim + c] = o;
+    *reinterpret_cast<v4f*>(reinterpret_cast<float*>(out) + off) = acc * inv;
   }
 }
 
