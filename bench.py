@@ -47,24 +47,35 @@ def causal_flops(B, Hq, L, D):
     return 4.0 * D * Hq * B * L * (L + 1) / 2.0
 
 
-def attn_src_digest():
+def src_digest(*names):
+    """sha256 prefix of kernel sources (and the device headers they include)."""
     h = hashlib.sha256()
-    with open(os.path.join(ROOT, "paper_2608_27875_amd", "csrc", "attn_prefill.hip"), "rb") as f:
-        h.update(f.read())
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2608_27875_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def load_traffic(workload):
-    """HBM bytes per attention launch from rocprofv3 FETCH_SIZE / WRITE_SIZE
-    counters (profiles/attn_traffic.json), only if taken on this kernel source."""
-    p = os.path.join(ROOT, "profiles", "attn_traffic.json")
+def attn_src_digest():
+    return src_digest("attn_prefill.hip", "codes_dev.h", "hyq_internal.h")
+
+
+def decode_src_digest():
+    return src_digest("decode.hip", "codes_dev.h", "quant_dev.h", "hyq_internal.h")
+
+
+def load_traffic(workload, fname="attn_traffic.json", digest=None):
+    """HBM bytes per kernel launch from rocprofv3 FETCH_SIZE / WRITE_SIZE
+    counters (profiles/<fname>), only if taken on this kernel source."""
+    p = os.path.join(ROOT, "profiles", fname)
     if not os.path.exists(p):
         return None
     try:
         rec = json.load(open(p))
     except ValueError:
         return None
-    if rec.get("kernel_src_sha") != attn_src_digest() or rec.get("workload") != workload:
+    if rec.get("kernel_src_sha") != (digest or attn_src_digest)() or \
+            rec.get("workload") != workload:
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -123,7 +134,7 @@ def decode_bytes(c, B):
 
 
 def decode_record(B, layers, steps, budget_ppm=50000, bits=4, N=32768, W=128, Hq=32, Hkv=8,
-                  seed=0, label=None):
+                  seed=0, label=None, probe=False):
     """Freeze `layers` synthetic layers, then time hyq_decode_attn over all of
     them (one decode token of a `layers`-layer model)."""
     import numpy as np
@@ -152,6 +163,20 @@ def decode_record(B, layers, steps, budget_ppm=50000, bits=4, N=32768, W=128, Hq
     def one_token():
         for c, q, o in zip(caches, qs, outs):
             hyq.hyq_decode_attn(c, q, o)   # on the current stream (the capture stream below)
+
+    if probe:   # for rocprofv3 --pmc: one token, the 1 GiB copy kernel, one more token
+        one_token()
+        n = 1 << 28
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        one_token()
+        torch.cuda.synchronize()
+        print(f"[bench] decode traffic probe done: {layers} layers x 2 tokens; copy kernel reads "
+              f"and writes {4 * n} bytes", file=sys.stderr, flush=True)
+        return None
 
     def timed(run):
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -193,8 +218,8 @@ def decode_record(B, layers, steps, budget_ppm=50000, bits=4, N=32768, W=128, Hq
     us_layer = ms * 1e3 / layers
     nbytes = decode_bytes(caches[0].c, B)
     gbs = nbytes / (us_layer * 1e-6) / 1e9
-    rec = {"workload": label or (f"decode_gqa{Hq}q{Hkv}kv_d128_B{B}_N{N}_W{W}_r{budget_ppm}ppm_"
-                                 f"kv{bits}bit"),
+    workload = label or f"decode_gqa{Hq}q{Hkv}kv_d128_B{B}_N{N}_W{W}_r{budget_ppm}ppm_kv{bits}bit"
+    rec = {"workload": workload,
            "layers": layers, "us_per_layer": round(us_layer, 3),
            "timing": "hip graph of the layer loop" if graph_ok else "eager launches",
            "us_per_layer_eager": round(ms_eager * 1e3 / layers, 3),
@@ -202,6 +227,7 @@ def decode_record(B, layers, steps, budget_ppm=50000, bits=4, N=32768, W=128, Hq
            "bytes_per_layer": int(nbytes),
            "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
                         "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                        "traffic": load_traffic(workload, "decode_traffic.json", decode_src_digest),
                         "kernel": "decode_attn_kernel + decode_combine_kernel"}}
     del caches, qs, outs
     torch.cuda.empty_cache()
@@ -267,6 +293,9 @@ def main():
     from paper_2608_27875_amd import gen
 
     if args.decode_only:
+        if args.traffic_probe:
+            decode_record(1, args.decode_layers, 1, probe=True)
+            return
         print(json.dumps({"decode": decode_section(args.decode_layers, args.steps)}), flush=True)
         return
 
