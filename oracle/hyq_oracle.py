@@ -333,19 +333,42 @@ def quantize(Qb, Kb, Vb, idx, W: int, bits: int, block: int = 64, fmt: str = "in
 # Eq. (prefill_hybrid): hybrid-precision causal attention
 # ---------------------------------------------------------------------------
 
-def _head_operands(Qb, Kb, Vb, b, h, Hkv, W, bits, block, idx, qz):
-    """Logit ingredients of one (batch, query head): for every key, its
-    original position, and the pieces of its logit and value."""
+WINDOW_MODES = ("fixed", "band")
+
+
+def _head_operands(Qb, Kb, Vb, b, h, Hkv, W, bits, block, idx, qz, window_mode="fixed"):
+    """Logit ingredients of one (batch, query head): for every key, the rows
+    that see it (lo <= t <= hi, original positions), and the pieces of its
+    logit and value.
+
+    window_mode "fixed": the full-precision window is the last W keys [P, L)
+    (Algorithms 1, 2, 4); a key is seen by every row t >= its position.
+    window_mode "band": the per-query window of eq. (win_def) with t0 = t + 1,
+    i.e. row t sees keys [t + 1 - W, t] in full precision; other keys of the
+    non-window prefix only quantized (position <= t - W); vertical lines in
+    full precision from their position on (eq. pre_def: the prefix is the
+    complement of the window of the current query).
+    """
     B, Hq, L, D = Qb.shape
     g = Hq // Hkv
     j = h // g
     P = max(0, L - W)
+    big = np.iinfo(np.int64).max
     if bits == 16:
         fp_pos = np.arange(L)
-    else:
+        fp_hi = np.full(L, big)
+    elif window_mode == "fixed":
         fp_pos = np.concatenate([idx[b, j].astype(np.int64), np.arange(P, L)])
+        fp_hi = np.full(len(fp_pos), big)
+    else:
+        vlp = idx[b, j].astype(np.int64)
+        rest = np.setdiff1d(np.arange(L), vlp)            # every non-vertical key, ascending
+        fp_pos = np.concatenate([vlp, rest])
+        fp_hi = np.concatenate([np.full(len(vlp), big), rest + W - 1])
     ops = dict(
         fp_pos=fp_pos,
+        fp_lo=fp_pos,
+        fp_hi=fp_hi,
         Q=bf16_to_f32(Qb[b, h]).astype(np.float64),
         Kfp=bf16_to_f32(Kb[b, j][fp_pos]).astype(np.float64),
         Vfp=bf16_to_f32(Vb[b, j][fp_pos]).astype(np.float64),
@@ -354,8 +377,10 @@ def _head_operands(Qb, Kb, Vb, b, h, Hkv, W, bits, block, idx, qz):
         nQ = qz["kq_pos"].shape[2]
         blk = np.arange(nQ) // block
         fmt = qz.get("fmt", "int")
+        q_pos = qz["kq_pos"][b, j].astype(np.int64)
         ops.update(
-            q_pos=qz["kq_pos"][b, j].astype(np.int64),
+            q_pos=q_pos,
+            q_lo=q_pos + (W if window_mode == "band" else 0),
             qcode=code_values(qz["q_codes"][b, h], fmt),
             qscale=qz["q_scale"][b, h].astype(np.float64),
             kcode=code_values(qz["k_codes"][b, j], fmt),
@@ -366,29 +391,37 @@ def _head_operands(Qb, Kb, Vb, b, h, Hkv, W, bits, block, idx, qz):
 
 
 def _rows_logits(ops, rows, D, bits, block):
-    """Concatenated logits [len(rows), nkeys], values and key positions."""
+    """Concatenated logits [len(rows), nkeys], values, key positions and the
+    first / last row that sees each key."""
     alpha = 1.0 / math.sqrt(D)
     Zfp = alpha * (ops["Q"][rows] @ ops["Kfp"].T)
     if bits == 16:
-        return Zfp, ops["Vfp"], ops["fp_pos"]
+        return Zfp, ops["Vfp"], ops["fp_pos"], ops["fp_lo"], ops["fp_hi"]
     # Quantized keys: alpha * s_Q * s_K * <q_code, k_code> (Algorithm 2, Segment A).
     Zq = alpha * (ops["qcode"][rows] @ ops["kcode"].T) \
         * ops["qscale"][rows // block][:, None] * ops["kscale"][None, :]
     Z = np.concatenate([Zq, Zfp], axis=1)
     Vall = np.concatenate([ops["vhat"], ops["Vfp"]], axis=0)
     pos = np.concatenate([ops["q_pos"], ops["fp_pos"]])
-    return Z, Vall, pos
+    lo = np.concatenate([ops["q_lo"], ops["fp_lo"]])
+    hi = np.concatenate([np.full(len(ops["q_pos"]), np.iinfo(np.int64).max), ops["fp_hi"]])
+    return Z, Vall, pos, lo, hi
 
 
 def attention(Qb, Kb, Vb, W: int, bits: int, idx, qz=None, block: int = 64,
-              heads=None, rows=None, return_weights: bool = False, chunk: int = 1024):
+              heads=None, rows=None, return_weights: bool = False, chunk: int = 1024,
+              window_mode: str = "fixed"):
     """Causal hybrid attention output in float32.
 
     ``heads``: list of (b, h) to evaluate (default: all); ``rows``: query rows
-    (default: all), shared by every listed head.  Returns O [len(heads),
-    len(rows), D] float32 (and, if ``return_weights``, the float64 weight
-    matrices over original key positions [len(heads), len(rows), L]).
+    (default: all), shared by every listed head.  ``window_mode``: "fixed"
+    or "band" (see _head_operands).  Returns O [len(heads), len(rows), D]
+    float32 (and, if ``return_weights``, the float64 weight matrices over
+    original key positions [len(heads), len(rows), L]; in band mode a
+    position's quantized and full-precision weights are added).
     """
+    if window_mode not in WINDOW_MODES:
+        raise ValueError(f"window_mode must be one of {WINDOW_MODES}")
     B, Hq, L, D = Qb.shape
     Hkv = Kb.shape[1]
     if heads is None:
@@ -396,27 +429,98 @@ def attention(Qb, Kb, Vb, W: int, bits: int, idx, qz=None, block: int = 64,
     rows = np.arange(L) if rows is None else np.asarray(rows, dtype=np.int64)
     O = np.zeros((len(heads), len(rows), D), dtype=np.float32)
     Wfull = np.zeros((len(heads), len(rows), L)) if return_weights else None
-    for hi, (b, h) in enumerate(heads):
-        ops = _head_operands(Qb, Kb, Vb, b, h, Hkv, W, bits, block, idx, qz)
-        for c0 in range(0, len(rows), chunk):
-            r = rows[c0:c0 + chunk]
-            Z, Vall, pos = _rows_logits(ops, r, D, bits, block)
-            Z = np.where(pos[None, :] <= r[:, None], Z, -np.inf)     # causal, original positions
+    for hi_, (b, h) in enumerate(heads):
+        ops = _head_operands(Qb, Kb, Vb, b, h, Hkv, W, bits, block, idx, qz, window_mode)
+        nkeys = len(ops["fp_pos"]) + (len(ops["q_pos"]) if bits != 16 else 0)
+        step = max(1, min(chunk, (1 << 25) // max(1, nkeys)))
+        for c0 in range(0, len(rows), step):
+            r = rows[c0:c0 + step]
+            Z, Vall, pos, lo, hi = _rows_logits(ops, r, D, bits, block)
+            seen = (lo[None, :] <= r[:, None]) & (r[:, None] <= hi[None, :])
+            Z = np.where(seen, Z, -np.inf)     # causal (and band), original positions
             m = Z.max(axis=1, keepdims=True)
             E = np.exp(Z - m)
             den = E.sum(axis=1, keepdims=True)
-            O[hi, c0:c0 + len(r)] = ((E @ Vall) / den).astype(np.float32)
+            O[hi_, c0:c0 + len(r)] = ((E @ Vall) / den).astype(np.float32)
             if return_weights:
-                Wfull[hi, c0:c0 + len(r)][:, pos] = E / den
+                Wr = np.zeros((len(r), L))
+                for kk in range(len(pos)):
+                    Wr[:, pos[kk]] += E[:, kk] / den[:, 0]
+                Wfull[hi_, c0:c0 + len(r)] = Wr
     return (O, Wfull) if return_weights else O
 
 
+def attention_final_chunk(Qb, Kb, Vb, W: int, bits: int, idx, qz, block: int = 64,
+                          tile: int = 64, heads=None):
+    """Algorithm 2, Stage 3 taken literally for the final query chunk, the
+    rows [L - W, L) (at most W rows): segment A (every quantized key) and
+    segment B (every vertical-line key) without a mask, segment C (the window
+    [L - W, L)) with the per-row causal mask; each segment scanned in tiles
+    of ``tile`` keys with the online-softmax update FlashOS (running max m,
+    sum l, accumulator), float64.  Returns O [len(heads), W', D] float32,
+    W' = min(W, L)."""
+    B, Hq, L, D = Qb.shape
+    Hkv = Kb.shape[1]
+    g = Hq // Hkv
+    P = max(0, L - W)
+    rows = np.arange(P, L)
+    alpha = 1.0 / math.sqrt(D)
+    if heads is None:
+        heads = [(b, h) for b in range(B) for h in range(Hq)]
+    O = np.zeros((len(heads), len(rows), D), dtype=np.float32)
+    for hi_, (b, h) in enumerate(heads):
+        j = h // g
+        q = bf16_to_f32(Qb[b, h][rows]).astype(np.float64)
+        Kf = bf16_to_f32(Kb[b, j]).astype(np.float64)
+        Vf = bf16_to_f32(Vb[b, j]).astype(np.float64)
+        m = np.full(len(rows), -np.inf)
+        l = np.zeros(len(rows))
+        acc = np.zeros((len(rows), D))
+
+        def flash_os(z, v):
+            nonlocal m, l, acc
+            mn = np.maximum(m, z.max(axis=1))
+            safe = np.where(np.isfinite(mn), mn, 0.0)
+            corr = np.where(np.isfinite(m), np.exp(m - safe), 0.0)
+            p = np.exp(z - safe[:, None])
+            l = l * corr + p.sum(axis=1)
+            acc = acc * corr[:, None] + p @ v
+            m = mn
+
+        if bits != 16:
+            fmt = qz.get("fmt", "int")
+            nQ = qz["kq_pos"].shape[2]
+            qcode = code_values(qz["q_codes"][b, h][rows], fmt)
+            qs = qz["q_scale"][b, h][rows // block].astype(np.float64)
+            kcode = code_values(qz["k_codes"][b, j], fmt)
+            vcode = code_values(qz["v_codes"][b, j], fmt)
+            for t0 in range(0, nQ, tile):                  # segment A, no mask
+                n = np.arange(t0, min(nQ, t0 + tile))
+                ks = qz["k_scale"][b, j][n // block].astype(np.float64)
+                vs = qz["v_scale"][b, j][n // block].astype(np.float64)
+                z = alpha * (qcode @ kcode[n].T) * qs[:, None] * ks[None, :]
+                flash_os(z, vs[:, None] * vcode[n])
+            vlp = idx[b, j].astype(np.int64)
+            for t0 in range(0, len(vlp), tile):            # segment B, no mask
+                pp = vlp[t0:t0 + tile]
+                flash_os(alpha * (q @ Kf[pp].T), Vf[pp])
+        win = np.arange(P, L) if bits != 16 else np.arange(0, L)
+        for t0 in range(0, len(win), tile):               # segment C, causal
+            pp = win[t0:t0 + tile]
+            z = alpha * (q @ Kf[pp].T)
+            z = np.where(pp[None, :] <= rows[:, None], z, -np.inf)
+            flash_os(z, Vf[pp])
+        O[hi_] = (acc / l[:, None]).astype(np.float32)
+    return O
+
+
 def prefill(Qb, Kb, Vb, Hkv: int, W: int, budget_ppm: int, bits: int, block: int = 64,
-            heads=None, rows=None, fmt: str = "int"):
+            heads=None, rows=None, fmt: str = "int", window_mode: str = "fixed"):
     """The whole path of Algorithm 2: selection, quantization, attention."""
     idx, _ = select_vertical(Qb, Kb, Hkv, W, budget_ppm)
     qz = quantize(Qb, Kb, Vb, idx, W, bits, block, fmt)
-    O = attention(Qb, Kb, Vb, W, bits, idx, qz, block, heads=heads, rows=rows)
+    O = attention(Qb, Kb, Vb, W, bits, idx, qz, block, heads=heads, rows=rows,
+                  window_mode=window_mode)
     return dict(idx=idx, O=O, **qz)
 
 

@@ -125,8 +125,11 @@ def topk_by_rank(S, k: int):
 
 
 def attention_rows(Qv, Kv, Vv, L, W, bits, block, idx_list, qcodes, qscales,
-                   kcodes, kscales, vcodes, vscales, fp8: bool = False):
+                   kcodes, kscales, vcodes, vscales, fp8: bool = False, band: bool = False):
     """Scalar-loop hybrid attention for one (batch, head).
+
+    band: the per-query window (row t sees keys t+1-W .. t in full precision,
+    a quantizable key only quantized when it is older than that).
 
     Qv, Kv, Vv: lists of float rows (original positions).  idx_list: the
     vertical positions of this KV head.  q/k/v codes and scales are per
@@ -146,7 +149,7 @@ def attention_rows(Qv, Kv, Vv, L, W, bits, block, idx_list, qcodes, qscales,
     for t in range(L):
         zs, vals, poss = [], [], []
         for p in range(t + 1):
-            if bits != 16 and p in where:
+            if bits != 16 and p in where and not (band and p >= t + 1 - W):
                 n = where[p]
                 dot = math.fsum(cv(qcodes[t][d]) * cv(kcodes[n][d]) for d in range(D))
                 z = alpha * qscales[t // block] * kscales[n] * dot

@@ -53,7 +53,7 @@ def test_exact_attention_float64_internals():
     qz = orc.quantize(d["Q"], d["K"], d["V"], idx, 8, 16)
     ops = orc._head_operands(d["Q"], d["K"], d["V"], 0, 1, 1, 8, 16, 64, idx, qz)
     rows = np.arange(96)
-    Z, Vall, pos = orc._rows_logits(ops, rows, 16, 16, 64)
+    Z, Vall, pos, _, _ = orc._rows_logits(ops, rows, 16, 16, 64)
     Z = np.where(pos[None, :] <= rows[:, None], Z, -np.inf)
     E = np.exp(Z - Z.max(1, keepdims=True))
     O = (E @ Vall) / E.sum(1, keepdims=True)
