@@ -272,6 +272,8 @@ def main():
     ap.add_argument("--no-fp8", action="store_true",
                     help="skip the FP8-code run of the same inputs")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode measurement")
+    ap.add_argument("--no-band", action="store_true",
+                    help="skip the per-query window (band) attention on the same inputs")
     ap.add_argument("--decode-only", action="store_true",
                     help="only the decode measurement (printed as its own JSON line)")
     ap.add_argument("--decode-layers", type=int, default=36)
@@ -444,6 +446,32 @@ def main():
                "frac_fp8_peak": round(tf8 / INT8_PEAK_TOPS, 4)}
         del b8
 
+    # the same inputs and codes with the per-query window of eq. (win_def):
+    # attention only (selection and quantization are the same)
+    band = None
+    if not args.no_band and shape.bits_kv != 16:
+        sb = dataclasses.replace(shape, window_mode=hyq.WIN_BAND)
+        print("[bench] per-query window (band) attention", file=sys.stderr, flush=True)
+
+        def stepb():
+            hyq.hyq_attn_prefill(sb, Q, K, V, bufs["idx"], bufs["q_codes"], bufs["q_scale"],
+                                 bufs["k_codes"], bufs["k_scale"], bufs["v_codes"],
+                                 bufs["v_scale"], bufs["kq_pos"], scale, bufs["out"], out_dtype,
+                                 stream)
+        stepb()
+        torch.cuda.synchronize()
+        eb = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(10)]
+        for e in eb:
+            e[0].record(stream)
+            stepb()
+            e[1].record(stream)
+        torch.cuda.synchronize()
+        msb = float(np.median([e[0].elapsed_time(e[1]) for e in eb]))
+        tfb = causal_flops(shape.B, shape.Hq, shape.L, shape.D) / (msb * 1e-3) / 1e12
+        band = {"attention_ms_median": round(msb, 4), "tflops": round(tfb, 2),
+                "frac_int8_peak": round(tfb / INT8_PEAK_TOPS, 4)}
+
     flops = causal_flops(shape.B, shape.Hq, shape.L, shape.D)
     value = flops / (ms_step * 1e-3) / 1e12
     attn_tflops = flops / (attn_ms * 1e-3) / 1e12
@@ -496,6 +524,7 @@ def main():
                       "quantize": round(float(np.median(qnt)), 4)},
         "bits16_same_inputs": bits16,
         "fp8_same_inputs": fp8,
+        "band_window_same_inputs": band,
         "attention_tflops": round(attn_tflops, 2),
         "frac_int8_peak": round(attn_tflops / INT8_PEAK_TOPS, 4),
         "frac_blended_ceiling": round(attn_tflops / BLENDED_PEAK, 4),

@@ -62,6 +62,13 @@ extern "C" {
                            the value nearest to x / s (ties to even, saturating at
                            +-448, zero keeps the sign of x), s = max|x| / 448.     */
 
+/* Readings of the full-precision window (eq. win_def of Section 4.1). */
+#define HYQ_WIN_FIXED 0   /* the last W keys [L-W, L), as Algorithms 1, 2 and 4 use it */
+#define HYQ_WIN_BAND  1   /* per query row t: keys [t+1-W, t] (eq. win_def with t0 = t+1);
+                             quantizable keys older than the band are seen quantized.
+                             Affects hyq_attn_prefill only (selection, quantization and
+                             the decode cache use the fixed window).                  */
+
 typedef struct hyq_shape {
   int32_t B, Hq, Hkv, L, D;  /* batch, query heads, KV heads, sequence, head dim      */
   int32_t window;            /* W >= 0: full-precision window = last W keys          */
@@ -69,6 +76,7 @@ typedef struct hyq_shape {
   int32_t bits_kv;           /* 16 (no quantization), 8 (int8) or 4 (packed int4)   */
   int32_t block;             /* quantization block in tokens (64)                   */
   int32_t kv_format;         /* HYQ_FMT_INT or HYQ_FMT_FP8 (ignored when bits = 16) */
+  int32_t window_mode;       /* HYQ_WIN_FIXED or HYQ_WIN_BAND                       */
 } hyq_shape;
 
 typedef struct hyq_sizes {
@@ -149,6 +157,9 @@ HYQ_API int hyq_quantize(const hyq_shape* shape, const void* Q, const void* K, c
  *       value = v_scale[c] * v_code[n];
  *   - vertical-line key (idx) or window key ([P, L)), and every key when
  *     bits_kv = 16:  z = alpha * <Q[t], K[k]>, value = V[k] (bf16 inputs).
+ * With window_mode = HYQ_WIN_BAND the window of row t is [t+1-W, t]: a
+ * quantizable key k is taken in full precision (as above) when t+1-W <= k
+ * and quantized when k <= t - W; vertical lines and keys >= P as above.
  * alpha = softmax_scale (1/sqrt(D) for the paper's operator).
  * out: [B][Hq][L][D], float32 (out_dtype 0) or bf16 (out_dtype 1).
  * The quantization buffers (q_codes ... kq_pos) are the outputs of

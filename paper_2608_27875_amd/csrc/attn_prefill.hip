@@ -14,7 +14,11 @@
 //              window), 64 at a time gathered into LDS: S^T with the bf16
 //              MFMA; P V with the bf16 MFMA on bf16 V, P split into a high
 //              and a low bf16 part so that P keeps ~16 bits.
-// Causality is by original key position in every segment.
+// Causality is by original key position in every segment.  With the
+// per-query window (HYQ_WIN_BAND) row t sees keys t+1-W .. t in full
+// precision and a quantized key only once it is older than that: segment A
+// compares positions with t - W, and the full-precision list also carries the
+// quantizable keys of the workgroup's band, each seen by W rows.
 //
 // Register layout (32x32 MFMA, wave64): lane l, accumulator register r holds
 // row (r/4)*8 + (l/32)*4 + r%4 and column l%32.  With keys as rows (S^T),
@@ -107,7 +111,8 @@ struct QRing {
 struct FBuf {                       // one full-precision tile
   alignas(16) uint8_t k[kTile * kKPitchBf];
   alignas(16) uint8_t v[kVBytes];
-  int32_t pos[kTile];
+  int32_t pos[kTile];               // rows t >= pos see the key ...
+  int32_t hi[kTile];                // ... up to row hi
 };
 union Smem {
   QRing q;
@@ -356,14 +361,34 @@ __device__ __forceinline__ void stage_store(KBuf& kb, VBuf& vb, const StageRegs<
 // Stage full-precision tile: entries e0 .. e0+63 of the list
 // [vertical positions (nvl of them), then base, base+1, ...]; entries at or
 // beyond `count` are padding (position HYQ_KQ_POS_PAD, zero rows).
+// The full-precision key list of a workgroup: nvl vertical lines (idx, seen
+// from their position on), then nqb quantizable keys of the per-query band
+// (kq[nq0 ..], each seen by the W rows from its position on), then the
+// window positions base .. (seen from their position on; in band mode by W
+// rows, which is every later row).  Entries [e0, e0 + 64) are staged.
 __device__ __forceinline__ void stage_fp(FBuf& b, const uint16_t* __restrict__ Kh,
                                          const uint16_t* __restrict__ Vh,
-                                         const int32_t* __restrict__ vl, int nvl, int base,
-                                         int e0, int count, int L) {
+                                         const int32_t* __restrict__ vl, int nvl,
+                                         const int32_t* __restrict__ kq, int nq0, int nqb,
+                                         int base, int e0, int count, int L, int band_w) {
   const int tid = threadIdx.x;
   if (tid < kTile) {
     const int e = e0 + tid;
-    b.pos[tid] = e >= count ? HYQ_KQ_POS_PAD : (e < nvl ? vl[e] : base + (e - nvl));
+    int p = HYQ_KQ_POS_PAD, hi = -1;
+    if (e < count) {
+      if (e < nvl) {
+        p = vl[e];
+        hi = INT32_MAX;
+      } else if (e < nvl + nqb) {
+        p = kq[nq0 + (e - nvl)];
+        hi = p + band_w - 1;
+      } else {
+        p = base + (e - nvl - nqb);
+        hi = band_w > 0 ? p + band_w - 1 : INT32_MAX;
+      }
+    }
+    b.pos[tid] = p;
+    b.hi[tid] = hi;
   }
   __syncthreads();
 #pragma unroll
@@ -550,7 +575,7 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
                     const uint8_t* __restrict__ v_codes, const float* __restrict__ v_scale,
                     const int32_t* __restrict__ kq_pos, void* __restrict__ out, int Hq, int Hkv,
                     int nbj, int L, int P, int k, int nQ, int n_qblk, int n_kvblk,
-                    float alpha_log2e) {
+                    float alpha_log2e, int band_w) {
   __shared__ Smem sm;
   const int g = Hq / Hkv;
   const int lane = threadIdx.x & 63;
@@ -590,8 +615,11 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
 #pragma unroll
     for (int r = 0; r < 16; ++r) st.acc[dg][r] = 0.0f;
 
-  // Which keys are visible to rows up to t_last.
-  int nvl, nq_tiles, fp_count, fp_base;
+  // Which keys are visible to rows up to t_last.  A quantized key at
+  // position p is seen by rows t >= p + shift: shift = 0 for the fixed window,
+  // W for the per-query band (whose rows see p in full precision instead).
+  const int shift = BITS == 16 ? 0 : band_w;
+  int nvl, nq_tiles, fp_count, fp_base, nq0 = 0, nqb = 0;
   float vref = 1.0f;
   if (BITS == 16) {
     nvl = 0;
@@ -600,10 +628,22 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
     fp_count = t_last + 1;
   } else {
     nvl = count_le(vl, k, t_last);
-    const int nq_vis = t_last < P ? (t_last + 1) - nvl : nQ;
+    const int tq_last = t_last - shift;        // last quantized position any row sees
+    const int nq_vis = tq_last < 0 ? 0 : (tq_last < P ? (tq_last + 1) - count_le(vl, k, tq_last) : nQ);
     nq_tiles = min((nq_vis + kTile - 1) / kTile, n_kvblk);
     fp_base = P;
-    fp_count = nvl + max(0, t_last + 1 - P);
+    if (band_w > 0) {
+      // band keys of the workgroup's rows: positions [lo, t_last], lo from its first row
+      const int t0_wg = ((wgi * kWaves) / g) * kRows;
+      const int lo = max(0, t0_wg + 1 - band_w);
+      const int hi_q = min(t_last, P - 1);    // quantizable band keys: non-vertical in [lo, hi_q]
+      if (lo <= hi_q) {
+        nq0 = lo - count_le(vl, k, lo - 1);    // non-vertical positions below lo
+        nqb = (hi_q + 1) - count_le(vl, k, hi_q) - nq0;
+      }
+      fp_base = max(P, lo);
+    }
+    fp_count = nvl + nqb + max(0, t_last + 1 - fp_base);
     // sVref: smallest power of two >= every V scale of this head
     float mx = 0.0f;
     for (int i = lane; i < n_kvblk; i += 64) mx = fmaxf(mx, v_scale[(size_t)bj * n_kvblk + i]);
@@ -631,7 +671,7 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
     a.ks0 = k_scale + (size_t)bj * n_kvblk;
     a.vs0 = v_scale + (size_t)bj * n_kvblk;
     a.n = nq_tiles;
-    a.t0 = t0;
+    a.t0 = t0 - shift;   // rows t see quantized positions <= t - shift
     a.cq = alpha_log2e * q_scale[bh * n_qblk + t0 / kBlock];
     a.inv_vref = inv_vref;
     a.lane = lane;
@@ -701,7 +741,8 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
     FBuf& fb = sm.f;
     for (int ft = 0; ft < nft; ++ft) {
       __syncthreads();
-      stage_fp(fb, Kh, Vh, vl, nvl, fp_base, ft * kTile, fp_count, L);
+      stage_fp(fb, Kh, Vh, vl, nvl, kq_pos + (size_t)bj * n_kvblk * kTile, nq0, nqb, fp_base,
+               ft * kTile, fp_count, L, shift);
       __syncthreads();
       v8bf ka[2][8];
 #pragma unroll
@@ -725,7 +766,8 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
       for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const bool vis = fb.pos[key_of(kh, r, half)] <= tq;
+          const int e = key_of(kh, r, half);
+          const bool vis = (fb.pos[e] <= tq) & (tq <= fb.hi[e]);
           mt = fmaxf(mt, vis ? sf[kh][r] * alpha_log2e : -INFINITY);
         }
       lazy_max(st, xhalf_max(mt));
@@ -735,7 +777,8 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
       for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const bool vis = fb.pos[key_of(kh, r, half)] <= tq;
+          const int e = key_of(kh, r, half);
+          const bool vis = (fb.pos[e] <= tq) & (tq <= fb.hi[e]);
           const float ex = __builtin_amdgcn_exp2f(sf[kh][r] * alpha_log2e - st.m);
           const float pv = vis ? ex : 0.0f;
           ps += pv;
@@ -798,7 +841,8 @@ hipError_t launch_t(const hyq_shape& s, const hyq_sizes& z, const uint16_t* Q,
   const dim3 grid(wg_per_bj * nbj);
   attn_prefill_kernel<BITS, OB, FMT><<<grid, kThreads, 0, st>>>(
       Q, K, V, idx, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, kq_pos, out, s.Hq,
-      s.Hkv, nbj, s.L, z.P, z.k, z.nQ, z.n_qblk, z.n_kvblk, softmax_scale * kLog2e);
+      s.Hkv, nbj, s.L, z.P, z.k, z.nQ, z.n_qblk, z.n_kvblk, softmax_scale * kLog2e,
+      s.window_mode == HYQ_WIN_BAND ? s.window : 0);
   return hipGetLastError();
 }
 

@@ -47,6 +47,9 @@ int check_shape(const hyq_shape* s, hyq_sizes* z) {
     return fail(HYQ_EINVAL, "kv_format must be HYQ_FMT_INT or HYQ_FMT_FP8 (got %d)", s->kv_format);
   if (s->kv_format == HYQ_FMT_FP8 && s->bits_kv == 4)
     return fail(HYQ_EINVAL, "FP8 codes need bits_kv = 8 (got 4)");
+  if (s->window_mode != HYQ_WIN_FIXED && s->window_mode != HYQ_WIN_BAND)
+    return fail(HYQ_EINVAL, "window_mode must be HYQ_WIN_FIXED or HYQ_WIN_BAND (got %d)",
+                s->window_mode);
   if (s->D != hyq::kHeadDim)
     return fail(HYQ_EUNSUPPORTED, "head dim %d not supported (only %d)", s->D, hyq::kHeadDim);
   if (s->block != hyq::kBlock)

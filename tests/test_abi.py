@@ -72,6 +72,7 @@ def test_sizes_match_oracle(lib, L, W, ppm, bits):
     (dict(block=32), hyq.HYQ_EUNSUPPORTED), (dict(Hq=72, Hkv=8), hyq.HYQ_EUNSUPPORTED),
     (dict(kv_format=2), hyq.HYQ_EINVAL), (dict(kv_format=-1), hyq.HYQ_EINVAL),
     (dict(kv_format=hyq.FMT_FP8, bits_kv=4), hyq.HYQ_EINVAL),
+    (dict(window_mode=2), hyq.HYQ_EINVAL), (dict(window_mode=-1), hyq.HYQ_EINVAL),
 ])
 def test_bad_shapes_rejected(lib, kw, code):
     with pytest.raises(hyq.HyqError) as e:
@@ -122,6 +123,25 @@ def _dshape(**kw):
                 block=64)
     base.update(kw)
     return hyq.Shape(**base)
+
+
+def test_shape_struct_layout_matches_header(tmp_path):
+    import subprocess
+    names = [n for n, _ in hyq._Shape._fields_]
+    src = ['#include <stdio.h>', '#include <stddef.h>', '#include "hyq.h"', 'int main(void) {',
+           'printf("%zu\\n", sizeof(hyq_shape));']
+    src += [f'printf("%zu\\n", offsetof(hyq_shape, {n}));' for n in names]
+    src += ['printf("%d %d %d %d\\n", HYQ_WIN_FIXED, HYQ_WIN_BAND, HYQ_FMT_INT, HYQ_FMT_FP8);',
+            'return 0; }']
+    c = tmp_path / "shape.c"
+    c.write_text("\n".join(src))
+    exe = tmp_path / "shape"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(c), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split()
+    assert int(out[0]) == ctypes.sizeof(hyq._Shape)
+    assert [int(v) for v in out[1:1 + len(names)]] == [getattr(hyq._Shape, n).offset for n in names]
+    assert [int(v) for v in out[1 + len(names):]] == [hyq.WIN_FIXED, hyq.WIN_BAND, hyq.FMT_INT,
+                                                       hyq.FMT_FP8]
 
 
 def test_dcache_struct_layout_matches_header(tmp_path):
