@@ -227,6 +227,52 @@ def select_vertical(Qb: np.ndarray, Kb: np.ndarray, Hkv: int, W: int, budget_ppm
     return topk_ascending(S, k), S
 
 
+def column_mass(Qb: np.ndarray, Kb: np.ndarray, Hkv: int, W: int) -> np.ndarray:
+    """Eq. (vl_score): S[b, j, k] = sum over the considered queries of their
+    attention probability on key k, for every key k in [0, L) (float64).
+
+    The considered queries are the tail rows [L - t, L), t = min(W, L) (the
+    rows Algorithm 1 summarizes) of the g query heads of KV head j; each
+    probability is the plain causal softmax over keys <= the query's row of
+    alpha * <q, k> with the bf16 inputs, alpha = 1/sqrt(D)."""
+    B, Hq, L, D = Qb.shape
+    g = Hq // Hkv
+    t = min(W, L)
+    rows = np.arange(L - t, L)
+    alpha = 1.0 / math.sqrt(D)
+    S = np.zeros((B, Hkv, L))
+    for b in range(B):
+        for j in range(Hkv):
+            Kf = bf16_to_f32(Kb[b, j]).astype(np.float64)
+            for r in range(g):
+                q = bf16_to_f32(Qb[b, j * g + r][rows]).astype(np.float64)
+                Z = alpha * (q @ Kf.T)
+                Z = np.where(np.arange(L)[None, :] <= rows[:, None], Z, -np.inf)
+                E = np.exp(Z - Z.max(axis=1, keepdims=True))
+                S[b, j] += (E / E.sum(axis=1, keepdims=True)).sum(axis=0)
+    return S
+
+
+def select_vertical_colmass(Qb: np.ndarray, Kb: np.ndarray, Hkv: int, W: int, budget_ppm: int):
+    """Eq. (vl_topk) on the exact column-mass score of eq. (vl_score): the k
+    prefix keys [0, P) with the largest S (same budget k and tie rule as
+    Algorithm 1).  Returns (idx [B,Hkv,k] int32 ascending, S [B,Hkv,P]
+    float64 or None when k = 0)."""
+    B, Hq, L, D = Qb.shape
+    sz = sizes(L, W, budget_ppm)
+    P, k = sz["P"], sz["k"]
+    if k == 0:
+        return np.zeros((B, Hkv, 0), dtype=np.int32), None
+    if min(W, L) < 1:
+        raise ValueError("a vertical budget needs a window of at least one query")
+    S = column_mass(Qb, Kb, Hkv, W)[:, :, :P]
+    out = np.empty((B, Hkv, k), dtype=np.int32)
+    for ix in np.ndindex(B, Hkv):
+        order = np.argsort(-S[ix], kind="stable")
+        out[ix] = np.sort(order[:k]).astype(np.int32)
+    return out, S
+
+
 # ---------------------------------------------------------------------------
 # Algorithm 2, Stages 1-2: partition and per-block quantization
 # ---------------------------------------------------------------------------
