@@ -69,6 +69,13 @@ extern "C" {
                              Affects hyq_attn_prefill only (selection, quantization and
                              the decode cache use the fixed window).                  */
 
+/* Vertical-line scores (Section 4.1). */
+#define HYQ_SEL_PROXY   0   /* Algorithm 1: qsum . K, qsum the summed tail queries  */
+#define HYQ_SEL_COLMASS 1   /* eq. vl_score: the attention mass the tail queries put
+                               on each key (causal softmax, alpha = 1/sqrt(D), summed
+                               over the tail rows and the g heads); same budget, top-k
+                               and tie rule                                          */
+
 typedef struct hyq_shape {
   int32_t B, Hq, Hkv, L, D;  /* batch, query heads, KV heads, sequence, head dim      */
   int32_t window;            /* W >= 0: full-precision window = last W keys          */
@@ -77,6 +84,7 @@ typedef struct hyq_shape {
   int32_t block;             /* quantization block in tokens (64)                   */
   int32_t kv_format;         /* HYQ_FMT_INT or HYQ_FMT_FP8 (ignored when bits = 16) */
   int32_t window_mode;       /* HYQ_WIN_FIXED or HYQ_WIN_BAND                       */
+  int32_t selector;          /* HYQ_SEL_PROXY or HYQ_SEL_COLMASS                    */
 } hyq_shape;
 
 typedef struct hyq_sizes {
@@ -116,6 +124,11 @@ HYQ_API int hyq_sizes_for(const hyq_shape* shape, hyq_sizes* out);
  * scores:  optional float [B][Hkv][P] output of S (NULL: not written).
  * ws:      device workspace of at least sizes.select_ws_bytes bytes (may be
  *          NULL when that is 0); its contents are scratch.
+ * With selector = HYQ_SEL_COLMASS, S[b][j][p] is instead the column mass of
+ * eq. vl_score: the sum over the tail rows i in [L-t, L) and the g heads of
+ * group j of softmax_{k <= i}(alpha <Q[i], K[k]>)[p], computed with bf16
+ * MFMA products and float32 exponentials and sums (not bit-reproducible
+ * against another summation order; the top-k is the same kernel).
  * Errors:  HYQ_EINVAL also when W = 0 and k > 0 (no tail queries).
  */
 HYQ_API int hyq_select_vertical(const hyq_shape* shape, const void* Q, const void* K,

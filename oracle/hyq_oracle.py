@@ -594,7 +594,7 @@ DECODE_WS = 64
 
 
 def freeze(Qb, Kb, Vb, Hkv: int, W: int, budget_ppm: int, bits: int, block: int = 64,
-           fmt: str = "int"):
+           fmt: str = "int", selector: str = "proxy"):
     """Algorithm 4 on a prefill of N tokens (bf16 inputs).  Returns the hybrid
     cache as a dict of numpy arrays (per (b, j) lists where sizes can grow):
     quantized prefix (kq_pos, k/v codes and scales per block), vertical-line
@@ -604,7 +604,10 @@ def freeze(Qb, Kb, Vb, Hkv: int, W: int, budget_ppm: int, bits: int, block: int 
     B, Hq, N, D = Qb.shape
     if W < DECODE_WS or N < W:
         raise ValueError("decode needs W >= Ws (merges move Ws window tokens) and N >= W")
-    idx, _ = select_vertical(Qb, Kb, Hkv, W, budget_ppm)
+    if selector == "colmass":
+        idx, _ = select_vertical_colmass(Qb, Kb, Hkv, W, budget_ppm)
+    else:
+        idx, _ = select_vertical(Qb, Kb, Hkv, W, budget_ppm)
     qz = quantize(Qb, Kb, Vb, idx, W, bits, block, fmt)
     P = max(0, N - W)
     nq = qz["kq_pos"].shape[2]

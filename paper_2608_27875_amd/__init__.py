@@ -24,6 +24,7 @@ HYQ_OK, HYQ_EINVAL, HYQ_EUNSUPPORTED, HYQ_EHIP = 0, -1, -2, -3
 KQ_POS_PAD = 0x7FFFFFFF
 FMT_INT, FMT_FP8 = 0, 1       # hyq_shape.kv_format
 WIN_FIXED, WIN_BAND = 0, 1    # hyq_shape.window_mode
+SEL_PROXY, SEL_COLMASS = 0, 1  # hyq_shape.selector
 DECODE_WS = 64                # HYQ_DECODE_WS: staging buffer capacity
 EXPORTED = ("hyq_sizes_for", "hyq_select_vertical", "hyq_quantize", "hyq_attn_prefill",
             "hyq_strerror", "hyq_last_error", "hyq_dcache_init", "hyq_freeze",
@@ -39,7 +40,7 @@ class HyqError(RuntimeError):
 class _Shape(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("B", "Hq", "Hkv", "L", "D", "window", "budget_ppm", "bits_kv", "block",
-                 "kv_format", "window_mode")]
+                 "kv_format", "window_mode", "selector")]
 
 
 class _Sizes(ctypes.Structure):
@@ -82,6 +83,7 @@ class Shape:
     block: int = 64
     kv_format: int = 0      # FMT_INT or FMT_FP8
     window_mode: int = 0    # WIN_FIXED or WIN_BAND
+    selector: int = 0       # SEL_PROXY (Algorithm 1) or SEL_COLMASS (eq. vl_score)
 
     def c(self) -> _Shape:
         return _Shape(*[int(getattr(self, f.name)) for f in dataclasses.fields(self)])

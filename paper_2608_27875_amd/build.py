@@ -12,7 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libhyq.so")
-SOURCES = ["hyq_api.cpp", "select.hip", "quantize.hip", "attn_prefill.hip", "decode.hip"]
+SOURCES = ["hyq_api.cpp", "select.hip", "quantize.hip", "attn_prefill.hip", "decode.hip", "colmass.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

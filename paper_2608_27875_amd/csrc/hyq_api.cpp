@@ -47,6 +47,9 @@ int check_shape(const hyq_shape* s, hyq_sizes* z) {
     return fail(HYQ_EINVAL, "kv_format must be HYQ_FMT_INT or HYQ_FMT_FP8 (got %d)", s->kv_format);
   if (s->kv_format == HYQ_FMT_FP8 && s->bits_kv == 4)
     return fail(HYQ_EINVAL, "FP8 codes need bits_kv = 8 (got 4)");
+  if (s->selector != HYQ_SEL_PROXY && s->selector != HYQ_SEL_COLMASS)
+    return fail(HYQ_EINVAL, "selector must be HYQ_SEL_PROXY or HYQ_SEL_COLMASS (got %d)",
+                s->selector);
   if (s->window_mode != HYQ_WIN_FIXED && s->window_mode != HYQ_WIN_BAND)
     return fail(HYQ_EINVAL, "window_mode must be HYQ_WIN_FIXED or HYQ_WIN_BAND (got %d)",
                 s->window_mode);
@@ -93,7 +96,10 @@ int check_shape(const hyq_shape* s, hyq_sizes* z) {
     z->v_codes_bytes = B * Hkv * (size_t)z->n_kvblk * D * (size_t)(bs * s->bits_kv / 8);
     z->kv_scale_bytes = B * Hkv * (size_t)z->n_kvblk * 4;
   }
-  z->select_ws_bytes = k > 0 ? align256(B * Hkv * D * 4) + align256(z->scores_bytes) : 0;
+  z->select_ws_bytes = k > 0 ? align256(B * Hkv * D * 4) + align256(z->scores_bytes) +
+                                   (s->selector == HYQ_SEL_COLMASS
+                                        ? align256(hyq::colmass_ws_bytes(*s)) : 0)
+                             : 0;
   return HYQ_OK;
 }
 
@@ -220,12 +226,12 @@ HYQ_API int hyq_select_vertical(const hyq_shape* shape, const void* Q, const voi
     return fail(HYQ_EINVAL, "workspace too small: %zu bytes given, %zu needed", ws_bytes,
                 z.select_ws_bytes);
   float* qsum = static_cast<float*>(ws);
-  float* sc = scores ? scores
-                     : reinterpret_cast<float*>(static_cast<char*>(ws) +
-                                                align256((size_t)shape->B * shape->Hkv *
-                                                         shape->D * 4));
+  const size_t off_sc = align256((size_t)shape->B * shape->Hkv * shape->D * 4);
+  float* sc = scores ? scores : reinterpret_cast<float*>(static_cast<char*>(ws) + off_sc);
+  float* cm = reinterpret_cast<float*>(static_cast<char*>(ws) + off_sc +
+                                       align256(z.scores_bytes));
   return hip_status(hyq::launch_select(*shape, z, static_cast<const uint16_t*>(Q),
-                                       static_cast<const uint16_t*>(K), idx, sc, qsum,
+                                       static_cast<const uint16_t*>(K), idx, sc, qsum, cm,
                                        static_cast<hipStream_t>(stream)),
                     "hyq_select_vertical launch");
 }
@@ -317,10 +323,13 @@ HYQ_API int hyq_freeze(const hyq_shape* prefill, const void* Q, const void* K, c
   const int BHkv = prefill->B * prefill->Hkv;
   if (z.k > 0) {
     float* qsum = static_cast<float*>(ws);
-    float* sc = reinterpret_cast<float*>(static_cast<char*>(ws) +
-                                         align256((size_t)BHkv * prefill->D * 4));
+    const size_t off_sc = align256((size_t)BHkv * prefill->D * 4);
+    float* sc = reinterpret_cast<float*>(static_cast<char*>(ws) + off_sc);
+    float* cm = reinterpret_cast<float*>(static_cast<char*>(ws) + off_sc +
+                                         align256(z.scores_bytes));
     hipError_t e = hyq::launch_select(*prefill, z, static_cast<const uint16_t*>(Q),
-                                      static_cast<const uint16_t*>(K), cache->vl_pos, sc, qsum, st);
+                                      static_cast<const uint16_t*>(K), cache->vl_pos, sc, qsum,
+                                      cm, st);
     if (e != hipSuccess) return hip_status(e, "hyq_freeze selection launch");
   }
   if (cache->cap_blocks > 0) {

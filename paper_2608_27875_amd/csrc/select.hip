@@ -1,5 +1,7 @@
 // Vertical-line selection: Algorithm 1 (App. A.1, Vertical Token
 // Identification) of HyQuant, GQA-native, one vertical set per KV head.
+// (The exact column-mass score of eq. vl_score, HYQ_SEL_COLMASS, is computed
+// in colmass.hip; the top-k below serves both.)
 //
 //   1. tail proxy   qsum[b][j] = sum over the g heads of the group and the
 //                   last t = min(W, L) query rows (float32, pinned order);
@@ -222,15 +224,20 @@ topk_kernel(const float* __restrict__ S, int32_t* __restrict__ idx, int P, int k
 
 hipError_t launch_select(const hyq_shape& s, const hyq_sizes& z, const uint16_t* Q,
                          const uint16_t* K, int32_t* idx, float* scores, float* qsum,
-                         hipStream_t st) {
+                         float* cm_ws, hipStream_t st) {
   if (z.k == 0) return hipSuccess;
   const int g = s.Hq / s.Hkv;
   const int t = s.window < s.L ? s.window : s.L;
   const int BH = s.B * s.Hkv;
-  tail_proxy_kernel<<<BH, g * kHeadDim, g * kHeadDim * sizeof(float), st>>>(Q, qsum, s.Hq,
-                                                                              s.Hkv, s.L, t);
-  dim3 sg((z.P + 255) / 256, BH);
-  score_kernel<<<sg, 256, 0, st>>>(K, qsum, scores, s.L, z.P);
+  if (s.selector == HYQ_SEL_COLMASS) {
+    const hipError_t e = launch_colmass_scores(s, z, Q, K, scores, cm_ws, st);
+    if (e != hipSuccess) return e;
+  } else {
+    tail_proxy_kernel<<<BH, g * kHeadDim, g * kHeadDim * sizeof(float), st>>>(Q, qsum, s.Hq,
+                                                                                s.Hkv, s.L, t);
+    dim3 sg((z.P + 255) / 256, BH);
+    score_kernel<<<sg, 256, 0, st>>>(K, qsum, scores, s.L, z.P);
+  }
   topk_kernel<<<BH, kTopkThreads, 0, st>>>(scores, idx, z.P, z.k);
   return hipGetLastError();
 }
