@@ -274,6 +274,8 @@ def main():
     ap.add_argument("--no-decode", action="store_true", help="skip the decode measurement")
     ap.add_argument("--no-band", action="store_true",
                     help="skip the per-query window (band) attention on the same inputs")
+    ap.add_argument("--no-colmass", action="store_true",
+                    help="skip the exact column-mass selector on the same inputs")
     ap.add_argument("--decode-only", action="store_true",
                     help="only the decode measurement (printed as its own JSON line)")
     ap.add_argument("--decode-layers", type=int, default=36)
@@ -472,6 +474,44 @@ def main():
         band = {"attention_ms_median": round(msb, 4), "tflops": round(tfb, 2),
                 "frac_int8_peak": round(tfb / INT8_PEAK_TOPS, 4)}
 
+    # the same inputs through the exact column-mass selector of eq. (vl_score):
+    # selection only (its top-k feeds the same quantize and attention)
+    colmass = None
+    if not args.no_colmass and z["k"]:
+        sc = dataclasses.replace(shape, selector=hyq.SEL_COLMASS)
+        bc = hyq.alloc_buffers(sc, dev, out_dtype)
+        print("[bench] column-mass selector", file=sys.stderr, flush=True)
+
+        def stepc():
+            hyq.hyq_select_vertical(sc, Q, K, bc["idx"], None, bc["ws"], stream)
+        stepc()
+        torch.cuda.synchronize()
+        ec = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(10)]
+        for e in ec:
+            e[0].record(stream)
+            stepc()
+            e[1].record(stream)
+        torch.cuda.synchronize()
+        msc = float(np.median([e[0].elapsed_time(e[1]) for e in ec]))
+        # two QK^T passes over the tail rows: every causal key, then the prefix
+        tr = min(shape.window, shape.L)
+        rows = shape.B * shape.Hq * tr
+        cflops = 2.0 * shape.D * rows * ((shape.L - tr) + (tr + 1) / 2.0 + z["P"])
+        cidx = bc["idx"].cpu().numpy().reshape(-1, z["k"])
+        pidx = bufs["idx"].cpu().numpy().reshape(-1, z["k"])
+        crec, agree = [], []
+        for bj in range(shape.B * shape.Hkv):
+            pp = [p for p in d["planted"][bj].tolist() if p < z["P"]]
+            if pp:
+                crec.append(len(set(pp) & set(cidx[bj].tolist())) / min(len(pp), z["k"]))
+            agree.append(len(set(pidx[bj].tolist()) & set(cidx[bj].tolist())) / z["k"])
+        colmass = {"select_ms_median": round(msc, 4), "tflops": round(cflops / (msc * 1e-3) / 1e12, 2),
+                   "frac_bf16_peak": round(cflops / (msc * 1e-3) / 1e12 / F16_PEAK_TFLOPS, 4),
+                   "planted_recall": round(float(np.mean(crec)), 4) if crec else None,
+                   "overlap_with_tail_proxy": round(float(np.mean(agree)), 4)}
+        del bc
+
     flops = causal_flops(shape.B, shape.Hq, shape.L, shape.D)
     value = flops / (ms_step * 1e-3) / 1e12
     attn_tflops = flops / (attn_ms * 1e-3) / 1e12
@@ -525,6 +565,7 @@ def main():
         "bits16_same_inputs": bits16,
         "fp8_same_inputs": fp8,
         "band_window_same_inputs": band,
+        "colmass_selector_same_inputs": colmass,
         "attention_tflops": round(attn_tflops, 2),
         "frac_int8_peak": round(attn_tflops / INT8_PEAK_TOPS, 4),
         "frac_blended_ceiling": round(attn_tflops / BLENDED_PEAK, 4),
