@@ -40,6 +40,11 @@ path follows the same ones):
   value nearest to fl32(x / s), ties to the even code, saturating at +-448,
   the sign kept when the result is zero; Q, K_Q and V_Q all use it; codes
   are stored as their bit patterns (uint8);
+* FP4 (the 4-bit floating-point format of the low-precision bulk path): OCP
+  E2M1 (no infinities or NaN, largest finite 6) for K_Q and V_Q with
+  c_B = 6, the code the E2M1 value nearest to fl32(x / s), ties to the even
+  code, saturating at +-6, the sign kept when the result is zero; Q stays at
+  8 bits in E4M3 (as with 4-bit integers, whose Q is int8); codes 0..15;
 * causality holds by original key position in every segment;
 * bits = 16 disables quantization: every key takes the full-precision path.
 
@@ -62,7 +67,8 @@ import numpy as np
 C_INT8 = 127
 C_INT4 = 7
 C_FP8 = 448          # c_B for FP8 (Algorithm 2, Stage 2)
-FORMATS = ("int", "fp8")
+C_FP4 = 6            # c_B for FP4 E2M1: its largest finite value
+FORMATS = ("int", "fp8", "fp4")
 
 
 # ---------------------------------------------------------------------------
@@ -126,10 +132,57 @@ def e4m3_encode(y: np.ndarray) -> np.ndarray:
     return np.where(np.signbit(y), code | np.uint8(0x80), code).astype(np.uint8)
 
 
-def code_values(codes: np.ndarray, fmt: str) -> np.ndarray:
-    """The numbers the stored codes stand for (float64)."""
+def e2m1_values() -> np.ndarray:
+    """Values of the 16 FP4 E2M1 codes (the OCP microscaling element format):
+    bit 3 sign, bits 2..1 exponent with bias 1, bit 0 mantissa; exponent 0 is
+    subnormal (m/2); no infinities, no NaN; largest finite value 6."""
+    out = np.empty(16, dtype=np.float64)
+    for code in range(16):
+        sign = -1.0 if code & 0x8 else 1.0
+        e = (code >> 1) & 0x3
+        m = code & 0x1
+        out[code] = sign * (m / 2.0 if e == 0 else (1.0 + m / 2.0) * 2.0 ** (e - 1))
+    return out
+
+
+_E2M1 = e2m1_values()
+
+
+def e2m1_decode(codes: np.ndarray) -> np.ndarray:
+    """FP4 E2M1 codes (0..15) -> float64 values (exact)."""
+    return _E2M1[np.asarray(codes).astype(np.uint8) & 0xF]
+
+
+def e2m1_encode(y: np.ndarray) -> np.ndarray:
+    """float32 -> FP4 E2M1 codes (uint8, 0..15): the nearest of the eight
+    magnitudes 0, 0.5, 1, 1.5, 2, 3, 4, 6, ties to the even code, |y| beyond 6
+    saturating to 6, the sign bit kept when the result is zero."""
+    y = np.asarray(y, dtype=np.float32)
+    mags = _E2M1[:8]                          # codes 0..7, ascending
+    a = np.minimum(np.abs(y).astype(np.float64), 6.0)
+    d = np.abs(a[..., None] - mags)           # distance to every magnitude
+    best = d.min(axis=-1, keepdims=True)
+    # among the nearest, the even code (two nearest codes are always adjacent)
+    cand = np.where(d == best, np.arange(8), 99)
+    even = np.where(cand % 2 == 0, cand, 99).min(axis=-1)
+    code = np.where(even < 99, even, cand.min(axis=-1)).astype(np.uint8)
+    return np.where(np.signbit(y), code | np.uint8(0x8), code).astype(np.uint8)
+
+
+def q_code_values(codes: np.ndarray, fmt: str) -> np.ndarray:
+    """The numbers the stored Q codes stand for (float64): E4M3 for both
+    floating-point formats (FP4 keeps the query at 8 bits), else integers."""
+    if fmt in ("fp8", "fp4"):
+        return e4m3_decode(codes)
+    return np.asarray(codes).astype(np.float64)
+
+
+def kv_code_values(codes: np.ndarray, fmt: str) -> np.ndarray:
+    """The numbers the stored K/V codes stand for (float64)."""
     if fmt == "fp8":
         return e4m3_decode(codes)
+    if fmt == "fp4":
+        return e2m1_decode(codes)
     return np.asarray(codes).astype(np.float64)
 
 
@@ -326,17 +379,36 @@ def quantize_rows_fp8(x: np.ndarray, block: int):
     return codes.reshape(nb * block, D)[:n], scales
 
 
+def quantize_rows_fp4(x: np.ndarray, block: int):
+    """Per-block FP4 quantization of rows x [n, D] (float32): Algorithm 2
+    Stage 2 with B = FP4 E2M1, c_B = 6, s = fl32(max|x| / 6), code =
+    E2M1(fl32(x / s)); s = 0 gives codes 0.  Returns (codes uint8 [n, D] in
+    0..15, scales float32)."""
+    n, D = x.shape
+    nb = -(-n // block)
+    padded = np.zeros((nb * block, D), dtype=np.float32)
+    padded[:n] = x
+    blocks = padded.reshape(nb, block, D)
+    amax = np.abs(blocks).max(axis=(1, 2))
+    scales = (amax / np.float32(C_FP4)).astype(np.float32)
+    safe = np.where(scales == 0, np.float32(1.0), scales)
+    codes = e2m1_encode((blocks / safe[:, None, None]).astype(np.float32))
+    codes[scales == 0] = 0
+    return codes.reshape(nb * block, D)[:n], scales
+
+
 def quantize(Qb, Kb, Vb, idx, W: int, bits: int, block: int = 64, fmt: str = "int"):
     """Algorithm 2, Stages 1-2 on bf16 inputs.
 
     Returns a dict: kq_pos [B,Hkv,nQ]; q_codes [B,Hq,L,D], q_scale
     [B,Hq,n_qblk]; k_codes / v_codes [B,Hkv,nQ,D] (not packed), k_scale /
     v_scale [B,Hkv,n_kvblk].  ``fmt`` "int": int8 codes in [-c, c]; "fp8"
-    (bits must be 8): E4M3 bit patterns (uint8) for Q, K and V.  bits = 16
+    (bits must be 8): E4M3 bit patterns (uint8) for Q, K and V; "fp4" (bits
+    must be 4): E2M1 codes (uint8, 0..15) for K and V, E4M3 for Q.  bits = 16
     returns only kq_pos (nothing is quantized).
     """
-    if fmt not in FORMATS or (fmt == "fp8" and bits != 8):
-        raise ValueError("fmt must be 'int', or 'fp8' with bits = 8")
+    if fmt not in FORMATS or (fmt == "fp8" and bits != 8) or (fmt == "fp4" and bits != 4):
+        raise ValueError("fmt must be 'int', 'fp8' with bits = 8, or 'fp4' with bits = 4")
     B, Hq, L, D = Qb.shape
     Hkv = Kb.shape[1]
     P = max(0, L - W)
@@ -350,17 +422,26 @@ def quantize(Qb, Kb, Vb, idx, W: int, bits: int, block: int = 64, fmt: str = "in
     if fmt == "fp8":
         def qrows(x, c):
             return quantize_rows_fp8(x, block)
+        q_rows = qrows
+        ctype = np.uint8
+    elif fmt == "fp4":
+        def qrows(x, c):
+            return quantize_rows_fp4(x, block)
+
+        def q_rows(x, c):
+            return quantize_rows_fp8(x, block)
         ctype = np.uint8
     else:
         def qrows(x, c):
             return quantize_rows(x, block, c)
+        q_rows = qrows
         ctype = np.int8
     c = code_bound(bits)
     q_codes = np.zeros((B, Hq, L, D), ctype)
     q_scale = np.zeros((B, Hq, n_qblk), np.float32)
     for b in range(B):
         for h in range(Hq):
-            q_codes[b, h], q_scale[b, h] = qrows(bf16_to_f32(Qb[b, h]), C_INT8)
+            q_codes[b, h], q_scale[b, h] = q_rows(bf16_to_f32(Qb[b, h]), C_INT8)
     k_codes = np.zeros((B, Hkv, nQ, D), ctype)
     v_codes = np.zeros((B, Hkv, nQ, D), ctype)
     k_scale = np.zeros((B, Hkv, n_kvblk), np.float32)
@@ -427,11 +508,11 @@ def _head_operands(Qb, Kb, Vb, b, h, Hkv, W, bits, block, idx, qz, window_mode="
         ops.update(
             q_pos=q_pos,
             q_lo=q_pos + (W if window_mode == "band" else 0),
-            qcode=code_values(qz["q_codes"][b, h], fmt),
+            qcode=q_code_values(qz["q_codes"][b, h], fmt),
             qscale=qz["q_scale"][b, h].astype(np.float64),
-            kcode=code_values(qz["k_codes"][b, j], fmt),
+            kcode=kv_code_values(qz["k_codes"][b, j], fmt),
             kscale=qz["k_scale"][b, j][blk].astype(np.float64),
-            vhat=qz["v_scale"][b, j][blk].astype(np.float64)[:, None] * code_values(qz["v_codes"][b, j], fmt),
+            vhat=qz["v_scale"][b, j][blk].astype(np.float64)[:, None] * kv_code_values(qz["v_codes"][b, j], fmt),
         )
     return ops
 
@@ -536,10 +617,10 @@ def attention_final_chunk(Qb, Kb, Vb, W: int, bits: int, idx, qz, block: int = 6
         if bits != 16:
             fmt = qz.get("fmt", "int")
             nQ = qz["kq_pos"].shape[2]
-            qcode = code_values(qz["q_codes"][b, h][rows], fmt)
+            qcode = q_code_values(qz["q_codes"][b, h][rows], fmt)
             qs = qz["q_scale"][b, h][rows // block].astype(np.float64)
-            kcode = code_values(qz["k_codes"][b, j], fmt)
-            vcode = code_values(qz["v_codes"][b, j], fmt)
+            kcode = kv_code_values(qz["k_codes"][b, j], fmt)
+            vcode = kv_code_values(qz["v_codes"][b, j], fmt)
             for t0 in range(0, nQ, tile):                  # segment A, no mask
                 n = np.arange(t0, min(nQ, t0 + tile))
                 ks = qz["k_scale"][b, j][n // block].astype(np.float64)
@@ -640,6 +721,8 @@ def freeze(Qb, Kb, Vb, Hkv: int, W: int, budget_ppm: int, bits: int, block: int 
 def _quantize_block(rows_f32: np.ndarray, cache):
     if cache["fmt"] == "fp8":
         return quantize_rows_fp8(rows_f32, rows_f32.shape[0])
+    if cache["fmt"] == "fp4":
+        return quantize_rows_fp4(rows_f32, rows_f32.shape[0])
     return quantize_rows(rows_f32, rows_f32.shape[0], code_bound(cache["bits"]))
 
 
@@ -690,8 +773,8 @@ def decode_keys(cache, bj):
                                      cache["k_scales"][bj], cache["v_scales"][bj],
                                      cache["q_pos"][bj]):
         n = len(pos)
-        Ks.append(np.float64(ksc) * code_values(kc[:n], fmt))
-        Vs.append(np.float64(vsc) * code_values(vc[:n], fmt))
+        Ks.append(np.float64(ksc) * kv_code_values(kc[:n], fmt))
+        Vs.append(np.float64(vsc) * kv_code_values(vc[:n], fmt))
         Ps.append(np.asarray(pos, np.int64))
     for kk, vv, pp in ((cache["vl_k"][bj], cache["vl_v"][bj], cache["vl_pos"][bj]),
                        (cache["win_k"][bj], cache["win_v"][bj], cache["win_pos"][bj]),

@@ -112,6 +112,47 @@ def quant_block_fp8_exact(vals):
     return codes, float(s)
 
 
+def e2m1_value_exact(code: int) -> Fraction:
+    """OCP FP4 E2M1 code -> exact rational, from its fields: sign bit 3,
+    exponent bits 2..1 with bias 1, mantissa bit 0; exponent 0 is subnormal.
+    Written from the format definition, independently of the oracle."""
+    code = int(code) & 0xF
+    sign = -1 if code >> 3 else 1
+    e = (code >> 1) & 0x3
+    m = code & 0x1
+    if e == 0:
+        return sign * Fraction(m, 2)
+    return sign * (1 + Fraction(m, 2)) * Fraction(2) ** (e - 1)
+
+
+def e2m1_nearest(x: Fraction, negative: bool) -> int:
+    """Nearest E2M1 code to the exact value x by enumeration (ties to the even
+    code; beyond +-6 the nearest is +-6); sign bit from ``negative``."""
+    a = abs(x)
+    best, bd = None, None
+    for code in range(8):
+        d = abs(e2m1_value_exact(code) - a)
+        if bd is None or d < bd or (d == bd and code % 2 == 0 and best % 2 == 1):
+            best, bd = code, d
+    return best | (0x8 if negative else 0)
+
+
+def quant_block_fp4_exact(vals):
+    """FP4 block quantization with exact rationals: s = fl32(amax/6), code =
+    nearest E2M1 to fl32(x/s)."""
+    fr = [Fraction(float(v)) for v in vals]
+    amax = max(abs(v) for v in fr)
+    s = round_to_f32(amax / 6)
+    if s == 0:
+        return [0] * len(fr), 0.0
+    codes = []
+    for v, raw in zip(fr, vals):
+        y = round_to_f32(v / s)
+        negative = y < 0 or (y == 0 and math.copysign(1.0, float(raw)) < 0)
+        codes.append(e2m1_nearest(y, negative))
+    return codes, float(s)
+
+
 def topk_by_rank(S, k: int):
     """Position p is chosen iff fewer than k positions beat it, where p' beats p
     when S[p'] > S[p], or S[p'] == S[p] and p' < p.  Ascending output."""
@@ -125,11 +166,13 @@ def topk_by_rank(S, k: int):
 
 
 def attention_rows(Qv, Kv, Vv, L, W, bits, block, idx_list, qcodes, qscales,
-                   kcodes, kscales, vcodes, vscales, fp8: bool = False, band: bool = False):
+                   kcodes, kscales, vcodes, vscales, fp8: bool = False, band: bool = False,
+                   fp4: bool = False):
     """Scalar-loop hybrid attention for one (batch, head).
 
     band: the per-query window (row t sees keys t+1-W .. t in full precision,
     a quantizable key only quantized when it is older than that).
+    fp8: every code is E4M3; fp4: Q codes E4M3, K/V codes E2M1.
 
     Qv, Kv, Vv: lists of float rows (original positions).  idx_list: the
     vertical positions of this KV head.  q/k/v codes and scales are per
@@ -141,7 +184,12 @@ def attention_rows(Qv, Kv, Vv, L, W, bits, block, idx_list, qcodes, qscales,
     P = max(0, L - W)
     vl = set(idx_list)
 
+    def cq(code):
+        return float(e4m3_value_exact(code)) if (fp8 or fp4) else int(code)
+
     def cv(code):
+        if fp4:
+            return float(e2m1_value_exact(code))
         return float(e4m3_value_exact(code)) if fp8 else int(code)
     qpos = [p for p in range(P) if p not in vl]          # quantized keys, ascending
     where = {p: n for n, p in enumerate(qpos)}
@@ -151,7 +199,7 @@ def attention_rows(Qv, Kv, Vv, L, W, bits, block, idx_list, qcodes, qscales,
         for p in range(t + 1):
             if bits != 16 and p in where and not (band and p >= t + 1 - W):
                 n = where[p]
-                dot = math.fsum(cv(qcodes[t][d]) * cv(kcodes[n][d]) for d in range(D))
+                dot = math.fsum(cq(qcodes[t][d]) * cv(kcodes[n][d]) for d in range(D))
                 z = alpha * qscales[t // block] * kscales[n] * dot
                 val = [vscales[n] * cv(vcodes[n][d]) for d in range(D)]
             else:

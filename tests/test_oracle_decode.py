@@ -22,7 +22,7 @@ def _all_positions(cache, bj):
     return orc.decode_keys(cache, bj)[2]
 
 
-@pytest.mark.parametrize("fmt,bits", [("int", 8), ("int", 4), ("fp8", 8)])
+@pytest.mark.parametrize("fmt,bits", [("int", 8), ("int", 4), ("fp8", 8), ("fp4", 4)])
 def test_freeze_partition_and_reuse_of_prefill_steps(fmt, bits):
     N, W, ppm = 400, 96, 50000
     d = _prefill(1, 2, 4, 2, N, 16, W)
@@ -73,7 +73,7 @@ def test_decode_without_quantized_keys_is_exact_attention():
     assert len(c["k_blocks"][0]) == 1                # the merge happened at the 65th token
 
 
-@pytest.mark.parametrize("fmt,bits", [("int", 8), ("int", 4), ("fp8", 8)])
+@pytest.mark.parametrize("fmt,bits", [("int", 8), ("int", 4), ("fp8", 8), ("fp4", 4)])
 def test_merge_quantizes_the_oldest_window_block(fmt, bits):
     N, W, D = 300, 80, 8
     d = _prefill(4, 1, 2, 1, N, D, W)
@@ -95,6 +95,8 @@ def test_merge_quantizes_the_oldest_window_block(fmt, bits):
     x = gen.bf16_bits_to_f32(oldest_k).ravel()
     if fmt == "fp8":
         codes, s = brute.quant_block_fp8_exact(x)
+    elif fmt == "fp4":
+        codes, s = brute.quant_block_fp4_exact(x)
     else:
         codes, s = brute.quant_block_exact(x, orc.code_bound(bits))
     assert np.ravel(c["k_blocks"][0][-1]).tolist() == codes
@@ -103,7 +105,7 @@ def test_merge_quantizes_the_oldest_window_block(fmt, bits):
     np.testing.assert_array_equal(np.stack(c["win_k"][0][-64:]), np.stack(added[:64]))
 
 
-@pytest.mark.parametrize("fmt,bits", [("int", 8), ("fp8", 8)])
+@pytest.mark.parametrize("fmt,bits", [("int", 8), ("fp8", 8), ("fp4", 4)])
 def test_decode_attention_brute_force_tiny(fmt, bits):
     """Scalar-loop attention over the four buffers, dequantizing every code
     from its fields / integer value, with exact sums."""
@@ -117,6 +119,8 @@ def test_decode_attention_brute_force_tiny(fmt, bits):
     O = orc.decode_attention(q, c)
 
     def cval(code):
+        if fmt == "fp4":
+            return float(brute.e2m1_value_exact(code))
         return float(brute.e4m3_value_exact(code)) if fmt == "fp8" else int(code)
     keys, vals = [], []
     for kc, vc, ks, vs, pos in zip(c["k_blocks"][0], c["v_blocks"][0], c["k_scales"][0],
