@@ -55,12 +55,20 @@ extern "C" {
 
 #define HYQ_KQ_POS_PAD 0x7fffffff   /* kq_pos value of padding slots */
 
-/* Code formats of the quantized path (Algorithm 2 takes B in {INT8, FP8}). */
+/* Code formats of the quantized path (Algorithm 2 takes B in {INT8, FP8};
+   Section 4.2 names INT4/FP4 for the low-precision bulk path as well). */
 #define HYQ_FMT_INT 0   /* symmetric integer codes: int8 (c = 127) or int4 (c = 7) */
 #define HYQ_FMT_FP8 1   /* OCP FP8 E4M3 codes (c = 448) for Q, K and V; needs
                            bits_kv = 8.  Each code byte is the E4M3 bit pattern of
                            the value nearest to x / s (ties to even, saturating at
                            +-448, zero keeps the sign of x), s = max|x| / 448.     */
+#define HYQ_FMT_FP4 2   /* OCP FP4 E2M1 codes (c = 6) for K and V, needs bits_kv =
+                           4: the code of x is the E2M1 value nearest to x / s
+                           (ties to the even code, saturating at +-6, zero keeps
+                           the sign of x), s = max|x| / 6; codes are packed two
+                           per byte like int4 (element 2i in the low nibble).  Q
+                           keeps 8 bits as E4M3 codes exactly as with
+                           HYQ_FMT_FP8.                                          */
 
 /* Readings of the full-precision window (eq. win_def of Section 4.1). */
 #define HYQ_WIN_FIXED 0   /* the last W keys [L-W, L), as Algorithms 1, 2 and 4 use it */
@@ -82,7 +90,8 @@ typedef struct hyq_shape {
   int32_t budget_ppm;        /* vertical ratio r in parts per million, 0..1000000    */
   int32_t bits_kv;           /* 16 (no quantization), 8 (int8) or 4 (packed int4)   */
   int32_t block;             /* quantization block in tokens (64)                   */
-  int32_t kv_format;         /* HYQ_FMT_INT or HYQ_FMT_FP8 (ignored when bits = 16) */
+  int32_t kv_format;         /* HYQ_FMT_INT, HYQ_FMT_FP8 (bits 8) or HYQ_FMT_FP4 (bits
+                                4); ignored when bits = 16                          */
   int32_t window_mode;       /* HYQ_WIN_FIXED or HYQ_WIN_BAND                       */
   int32_t selector;          /* HYQ_SEL_PROXY or HYQ_SEL_COLMASS                    */
 } hyq_shape;
@@ -227,7 +236,7 @@ typedef struct hyq_dcache {
   int32_t B, Hq, Hkv, D;
   int32_t window;        /* W, 64 <= W <= N                                      */
   int32_t bits_kv;       /* 8 or 4                                               */
-  int32_t kv_format;     /* HYQ_FMT_INT or HYQ_FMT_FP8                           */
+  int32_t kv_format;     /* HYQ_FMT_INT, HYQ_FMT_FP8 (bits 8) or HYQ_FMT_FP4 (bits 4)*/
   int32_t n_vl;          /* k: vertical-line tokens per KV head                  */
   int32_t vl_rows;       /* k rounded up to a multiple of 64                     */
   int32_t ring_rows;     /* roundup(W, 64) + HYQ_DECODE_WS                       */

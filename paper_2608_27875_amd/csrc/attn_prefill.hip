@@ -8,8 +8,10 @@
 //   segment A: the quantized keys (compacted K_Q order) in tiles of 64 =
 //              one quantization block: S^T = K_codes * Qcodes^T with the int8
 //              MFMA (exact int32) or, for FP8 codes, the E4M3 MFMA (float32),
-//              logits scaled by alpha*log2(e)*sQ*sK; P V with the f16 MFMA
-//              on the V codes (int8 and E4M3 values are exact in f16);
+//              or, for FP4 codes, the scaled MFMA with E2M1 keys against
+//              E4M3 queries; logits scaled by alpha*log2(e)*sQ*sK; P V with
+//              the f16 MFMA on the V codes (int8, E4M3 and E2M1 values are
+//              exact in f16);
 //   segments B and C: the full-precision keys (vertical lines, then the
 //              window), 64 at a time gathered into LDS: S^T with the bf16
 //              MFMA; P V with the bf16 MFMA on bf16 V, P split into a high
@@ -160,6 +162,12 @@ __device__ __forceinline__ int vslot(int e) {
 __device__ __forceinline__ int kswz(int row, int chunk) {
   return row * kKRowI8 + ((chunk ^ ((row >> 1) & 7)) << 4);
 }
+// E2M1 K tile: 64 rows of 64 B (four 16-byte chunks); a 256-byte bank row
+// holds four K rows, so chunk j of row r sits at slot j ^ ((r / 4) % 4) and
+// the 16 rows of one read phase land on distinct banks.
+__device__ __forceinline__ int kswz4(int row, int chunk) {
+  return row * (kHeadDim / 2) + ((chunk ^ ((row >> 2) & 3)) << 4);
+}
 
 // (native vectors: aggregate copies of HIP's uint4 would go through memory)
 // Chunks per thread: 8-bit tiles split evenly; a 4-bit tile has one chunk for
@@ -187,6 +195,12 @@ struct StageRegs {
 // v_mfma_scale_f32_32x32x64_f8f6f4, lane half h holding channels
 // 64*step + 32h .. +32.  Q fragments (the B operands) split the channels the
 // same way, which is all the dot product needs.
+// E2M1 keys against E4M3 queries (2 steps of the same scaled MFMA): the
+// 4-bit A operand of lane half h takes the products 16h .. +16 and
+// 32 + 16h .. +16 of the step's 64, the 8-bit B operand of half h the
+// products 32h .. +32; channels are assigned so that the K fragment is the
+// 16 contiguous bytes of channels 64*step + 32h .. +32, and the Q fragment
+// the two 16-byte runs at channels 64*step + 16h and 64*step + 32 + 16h.
 template <int FMT>
 struct KFrag {
   v4i f[2][4];
@@ -195,12 +209,20 @@ template <>
 struct KFrag<HYQ_FMT_FP8> {
   v8i f[2][2];
 };
+template <>
+struct KFrag<HYQ_FMT_FP4> {
+  v4i f[2][2];
+};
 template <int FMT>
 struct QFrag {
   v4i f[4];
 };
 template <>
 struct QFrag<HYQ_FMT_FP8> {
+  v8i f[2];
+};
+template <>
+struct QFrag<HYQ_FMT_FP4> {
   v8i f[2];
 };
 
@@ -215,6 +237,10 @@ __device__ __forceinline__ void read_kfrag(KFrag<FMT>& kf, const KBuf& b, int co
         const v4i hi = *reinterpret_cast<const v4i*>(b.k + kswz(kh * 32 + col, kk * 4 + half * 2 + 1));
         kf.f[kh][kk] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       }
+    } else if constexpr (FMT == HYQ_FMT_FP4) {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+        kf.f[kh][kk] = *reinterpret_cast<const v4i*>(b.k + kswz4(kh * 32 + col, kk * 2 + half));
     } else {
 #pragma unroll
       for (int k4 = 0; k4 < 4; ++k4)
@@ -229,6 +255,13 @@ __device__ __forceinline__ void read_qfrag(QFrag<FMT>& qf, const int8_t* qrow, b
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
       qf.f[kk] = ok ? *reinterpret_cast<const v8i*>(qrow + kk * 64 + half * 32) : v8i{};
+  } else if constexpr (FMT == HYQ_FMT_FP4) {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const v4i lo = ok ? *reinterpret_cast<const v4i*>(qrow + kk * 64 + half * 16) : v4i{};
+      const v4i hi = ok ? *reinterpret_cast<const v4i*>(qrow + kk * 64 + 32 + half * 16) : v4i{};
+      qf.f[kk] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
   } else {
 #pragma unroll
     for (int k4 = 0; k4 < 4; ++k4)
@@ -236,9 +269,9 @@ __device__ __forceinline__ void read_qfrag(QFrag<FMT>& qf, const int8_t* qrow, b
   }
 }
 
-// S^T of one tile: int32 (int8 codes) or float32 (E4M3 codes) logits.
+// S^T of one tile: int32 (int8 codes) or float32 (E4M3, E2M1 codes) logits.
 template <int FMT>
-using SVec = std::conditional_t<FMT == HYQ_FMT_FP8, v16f, v16i>;
+using SVec = std::conditional_t<FMT == HYQ_FMT_INT, v16i, v16f>;
 
 template <int FMT>
 __device__ __forceinline__ void qk_tile(SVec<FMT> (&s)[2], const KFrag<FMT>& kf,
@@ -251,6 +284,13 @@ __device__ __forceinline__ void qk_tile(SVec<FMT> (&s)[2], const KFrag<FMT>& kf,
       for (int kk = 0; kk < 2; ++kk)   // format 0 = E4M3 for both operands, unit scales
         s[kh] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kf.f[kh][kk], qf.f[kk], s[kh], 0,
                                                                 0, 0, 127, 0, 127);
+    } else if constexpr (FMT == HYQ_FMT_FP4) {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {   // A format 4 = E2M1 (4 registers), B format 0 = E4M3
+        const v8i ka = __builtin_shufflevector(kf.f[kh][kk], v4i{}, 0, 1, 2, 3, 4, 5, 6, 7);
+        s[kh] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ka, qf.f[kk], s[kh], 4, 0, 0, 127,
+                                                                0, 127);
+      }
     } else {
 #pragma unroll
       for (int k4 = 0; k4 < 4; ++k4)
@@ -320,6 +360,23 @@ __device__ __forceinline__ void stage_store(KBuf& kb, VBuf& vb, const StageRegs<
       codes4_to_h<FMT>(w.z, h[4], h[5], vs);   // keys 8..11
       codes4_to_h<FMT>(w.w, h[6], h[7], vs);   // keys 12..15
       uint8_t* dst = vb.v + d * kVPitch + kg * 32;
+      *reinterpret_cast<v4u*>(dst) = v4u{h[0], h[1], h[4], h[5]};
+      *reinterpret_cast<v4u*>(dst + 16) = v4u{h[2], h[3], h[6], h[7]};
+    }
+  } else if constexpr (FMT == HYQ_FMT_FP4) {
+    // E2M1 K: the 16-byte chunk as it is (the MFMA reads 4-bit operands);
+    // V: E2M1 -> f16 times 2^e, two codes per conversion, exact
+    const int q4 = chunk_id<BITS>(tid, 0);
+    *reinterpret_cast<v4u*>(kb.k + kswz4(q4 >> 2, q4 & 3)) = r.k[0];
+    const int d = q4 >> 1, kh = q4 & 1;   // channel d, keys kh*32 .. +32 (16 B packed)
+    const v4u w = r.v[0];
+    const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int g16 = 0; g16 < 2; ++g16) {
+      uint32_t h[8];   // h[e]: keys 2e, 2e + 1 of the 16
+      e2m1x8_to_h(ww[2 * g16], *reinterpret_cast<uint32_t(*)[4]>(&h[0]), vs.f32);
+      e2m1x8_to_h(ww[2 * g16 + 1], *reinterpret_cast<uint32_t(*)[4]>(&h[4]), vs.f32);
+      uint8_t* dst = vb.v + d * kVPitch + (kh * 2 + g16) * 32;
       *reinterpret_cast<v4u*>(dst) = v4u{h[0], h[1], h[4], h[5]};
       *reinterpret_cast<v4u*>(dst + 16) = v4u{h[2], h[3], h[6], h[7]};
     }
@@ -501,7 +558,8 @@ template <int BITS, int FMT, int PH>
 __device__ __forceinline__ void segA_tile(Smem& sm, const SegA& a, int c, const QFrag<FMT>& qf,
                                           NState& st, const v8h (&pprev)[4], v8h (&pcur)[4],
                                           StageRegs<BITS>& sr, KFrag<FMT>& kf) {
-  constexpr float kSub = BITS == 8 ? 1.0f : 0.0625f;   // 4-bit codes are staged as 16*code
+  // 4-bit integer codes are staged as 16*code
+  constexpr float kSub = (BITS == 8 || FMT == HYQ_FMT_FP4) ? 1.0f : 0.0625f;
   const int tid = threadIdx.x;
   const KBuf& cur = sm.q.kb[PH];
   const VBuf& prv = sm.q.vb[(PH + 1) & 1];
@@ -649,7 +707,7 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
     for (int i = lane; i < n_kvblk; i += 64) mx = fmaxf(mx, v_scale[(size_t)bj * n_kvblk + i]);
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-    if (BITS == 4) mx *= 0.0625f;
+    if (BITS == 4 && FMT == HYQ_FMT_INT) mx *= 0.0625f;
     if (mx > 0.0f) {
       int e;
       frexpf(mx, &e);
@@ -861,6 +919,9 @@ hipError_t launch_attn_prefill(const hyq_shape& s, const hyq_sizes& z, const uin
   if (s.bits_kv == 16) {
     if (out_dtype) HYQ_LAUNCH(16, 1, HYQ_FMT_INT);
     HYQ_LAUNCH(16, 0, HYQ_FMT_INT);
+  } else if (s.bits_kv == 4 && s.kv_format == HYQ_FMT_FP4) {
+    if (out_dtype) HYQ_LAUNCH(4, 1, HYQ_FMT_FP4);
+    HYQ_LAUNCH(4, 0, HYQ_FMT_FP4);
   } else if (s.bits_kv == 8 && s.kv_format == HYQ_FMT_FP8) {
     if (out_dtype) HYQ_LAUNCH(8, 1, HYQ_FMT_FP8);
     HYQ_LAUNCH(8, 0, HYQ_FMT_FP8);

@@ -1,4 +1,5 @@
-// Device conversions of quantized codes (int8, packed int4, FP8 E4M3) to f16
+// Device conversions of quantized codes (int8, packed int4, FP8 E4M3, packed
+// FP4 E2M1) to f16
 // MFMA operands, shared by the prefill and decode attention kernels.  Every
 // conversion is exact: codes are small integers or E4M3 values, both exact in
 // f16, and the only scaling applied is by a power of two.
@@ -56,6 +57,16 @@ __device__ __forceinline__ void codes4_to_h(uint32_t w, uint32_t& h01, uint32_t&
                                             const VScale& vs) {
   if constexpr (FMT == HYQ_FMT_FP8) e4m3x4_to_h(w, h01, h23, vs);
   else i8x4_to_h(w, h01, h23, vs);
+}
+
+// Eight packed E2M1 codes (element 2i in the low nibble of byte i) -> f16
+// pairs (elements 2i, 2i+1 in h[i]) of value * p2, p2 a power of two: exact
+// unless the result is below the f16 range.
+__device__ __forceinline__ void e2m1x8_to_h(uint32_t w, uint32_t (&h)[4], float p2) {
+  h[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, p2, 0));
+  h[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, p2, 1));
+  h[2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, p2, 2));
+  h[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w, p2, 3));
 }
 
 // Packed int4 (8 nibbles, element 2i low / 2i+1 high in byte i) -> 8 int8 of

@@ -128,7 +128,7 @@ struct AppendArgs {
 template <int BITS, int FMT>
 __global__ void __launch_bounds__(kQuantThreads)
 append_kernel(AppendArgs a) {
-  constexpr float C = FMT == HYQ_FMT_FP8 ? 448.0f : (BITS == 8 ? 127.0f : 7.0f);
+  constexpr float C = code_bound<BITS, FMT>();
   constexpr int kRow = BITS == 8 ? kHeadDim : kHeadDim / 2;
   constexpr int vRow = BITS == 8 ? kBlock : kBlock / 2;
   __shared__ float red[kQuantThreads / 64];
@@ -280,6 +280,13 @@ __device__ __forceinline__ v8h i4x8_to_h_perm(uint32_t w, const I4Scale& s) {
   return v8h{ha[0], ha[1], hb[0], hb[1], hc[0], hc[1], hd[0], hd[1]};
 }
 
+// 8 packed E2M1 codes (one dword) -> their f16 values, element order.
+__device__ __forceinline__ v8h e2m1x8_to_h8(uint32_t w) {
+  uint32_t h[4];
+  e2m1x8_to_h(w, h, 1.0f);
+  return __builtin_bit_cast(v8h, v4u{h[0], h[1], h[2], h[3]});
+}
+
 // 8 one-byte codes (two dwords) -> f16 values code * 2^e, element order.
 template <int FMT>
 __device__ __forceinline__ v8h b8x8_to_h(uint32_t w0, uint32_t w1, const VScale& vs) {
@@ -308,7 +315,8 @@ __device__ __forceinline__ int unit_row(int t, int m) { return ((m >> 2) << 4) +
 // MFMA operand may be any set as long as both operands use the same one).
 // Each map makes the 4 lane groups of one load instruction read one
 // contiguous 64-byte run of a row:
-//   kMapI4:   int4 K rows (64 B): channels 32G + 8s .. (one 16-byte load);
+//   kMapI4:   int4 / E2M1 K rows (64 B): channels 32G + 8s .. (one 16-byte
+//             load);
 //   kMapB8:   int8 / E4M3 K rows (128 B): load u = s/2 holds channels
 //             64u + 16G .. +16, step s the half s%2 of it;
 //   kMapBF16: bf16 rows (256 B): channels 32s + 8G .. (one load per step).
@@ -416,7 +424,8 @@ __device__ __forceinline__ void process_block(WaveState& st, const QRegs<BITS>& 
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       v8h ka;
-      if constexpr (BITS == 4) ka = i4x8_to_h_perm(r.k[t][0][s], one4);
+      if constexpr (FMT == HYQ_FMT_FP4) ka = e2m1x8_to_h8(r.k[t][0][s]);
+      else if constexpr (BITS == 4) ka = i4x8_to_h_perm(r.k[t][0][s], one4);
       else ka = b8x8_to_h<FMT>(r.k[t][s >> 1][(s & 1) * 2], r.k[t][s >> 1][(s & 1) * 2 + 1], one8);
       sc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka, qh[s], sc[t], 0, 0, 0);
     }
@@ -460,7 +469,7 @@ __device__ __forceinline__ void process_block(WaveState& st, const QRegs<BITS>& 
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
     v8h pb;
-    if constexpr (BITS == 4) {
+    if constexpr (BITS == 4 && FMT == HYQ_FMT_INT) {   // the int4 conversion's key order
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         pb[2 * q] = p[(2 * s) * 4 + q];
@@ -476,7 +485,8 @@ __device__ __forceinline__ void process_block(WaveState& st, const QRegs<BITS>& 
 #pragma unroll
     for (int ct = 0; ct < 8; ++ct) {
       v8h va;
-      if constexpr (BITS == 4) va = i4x8_to_h_perm(r.v[ct][s], one4);
+      if constexpr (FMT == HYQ_FMT_FP4) va = e2m1x8_to_h8(r.v[ct][s]);
+      else if constexpr (BITS == 4) va = i4x8_to_h_perm(r.v[ct][s], one4);
       else va = b8x8_to_h<FMT>(r.v[ct][2 * s], r.v[ct][2 * s + 1], one8);
       st.acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb, st.acc[ct], 0, 0, 0);
     }
@@ -618,7 +628,7 @@ decode_attn_kernel(DecodeArgs a, const float* __restrict__ ks, const float* __re
         f[2 * e] = bf16_lo(qw[s][e]) * qmul;
         f[2 * e + 1] = bf16_hi(qw[s][e]) * qmul;
       }
-      if constexpr (BITS == 4) {
+      if constexpr (BITS == 4 && FMT == HYQ_FMT_INT) {   // the int4 conversion's order
         const int ord[8] = {0, 4, 1, 5, 2, 6, 3, 7};
 #pragma unroll
         for (int e = 0; e < 8; ++e) qh[s][e] = (_Float16)f[ord[e]];
@@ -825,7 +835,8 @@ hipError_t launch_decode_append(const hyq_dcache& c, const uint16_t* k_new, cons
   a.pos0 = (int)(c.t - c.n_staged - c.window);
   a.slot = slot;
   dim3 grid(c.B * c.Hkv, 2);
-  if (c.kv_format == HYQ_FMT_FP8) append_kernel<8, HYQ_FMT_FP8><<<grid, kQuantThreads, 0, st>>>(a);
+  if (c.kv_format == HYQ_FMT_FP4) append_kernel<4, HYQ_FMT_FP4><<<grid, kQuantThreads, 0, st>>>(a);
+  else if (c.kv_format == HYQ_FMT_FP8) append_kernel<8, HYQ_FMT_FP8><<<grid, kQuantThreads, 0, st>>>(a);
   else if (c.bits_kv == 8) append_kernel<8, HYQ_FMT_INT><<<grid, kQuantThreads, 0, st>>>(a);
   else append_kernel<4, HYQ_FMT_INT><<<grid, kQuantThreads, 0, st>>>(a);
   return hipGetLastError();
@@ -860,7 +871,9 @@ hipError_t launch_decode_attn(const hyq_dcache& c, const uint16_t* q, float soft
   a.c_log2 = softmax_scale * 1.4426950408889634f;
   const int S = d.S_q + d.S_f;
   dim3 grid(S, c.B * c.Hkv);
-  if (c.kv_format == HYQ_FMT_FP8)
+  if (c.kv_format == HYQ_FMT_FP4)
+    decode_attn_kernel<4, HYQ_FMT_FP4><<<grid, kDecThreads, 0, st>>>(a, c.k_scale, c.v_scale);
+  else if (c.kv_format == HYQ_FMT_FP8)
     decode_attn_kernel<8, HYQ_FMT_FP8><<<grid, kDecThreads, 0, st>>>(a, c.k_scale, c.v_scale);
   else if (c.bits_kv == 8)
     decode_attn_kernel<8, HYQ_FMT_INT><<<grid, kDecThreads, 0, st>>>(a, c.k_scale, c.v_scale);

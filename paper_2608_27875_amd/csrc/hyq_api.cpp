@@ -43,10 +43,13 @@ int check_shape(const hyq_shape* s, hyq_sizes* z) {
   if (s->block < 1) return fail(HYQ_EINVAL, "block must be >= 1 (got %d)", s->block);
   if (s->bits_kv != 16 && s->bits_kv != 8 && s->bits_kv != 4)
     return fail(HYQ_EUNSUPPORTED, "bits_kv must be 16, 8 or 4 (got %d)", s->bits_kv);
-  if (s->kv_format != HYQ_FMT_INT && s->kv_format != HYQ_FMT_FP8)
-    return fail(HYQ_EINVAL, "kv_format must be HYQ_FMT_INT or HYQ_FMT_FP8 (got %d)", s->kv_format);
+  if (s->kv_format != HYQ_FMT_INT && s->kv_format != HYQ_FMT_FP8 && s->kv_format != HYQ_FMT_FP4)
+    return fail(HYQ_EINVAL, "kv_format must be HYQ_FMT_INT, HYQ_FMT_FP8 or HYQ_FMT_FP4 (got %d)",
+                s->kv_format);
   if (s->kv_format == HYQ_FMT_FP8 && s->bits_kv == 4)
     return fail(HYQ_EINVAL, "FP8 codes need bits_kv = 8 (got 4)");
+  if (s->kv_format == HYQ_FMT_FP4 && s->bits_kv == 8)
+    return fail(HYQ_EINVAL, "FP4 codes need bits_kv = 4 (got 8)");
   if (s->selector != HYQ_SEL_PROXY && s->selector != HYQ_SEL_COLMASS)
     return fail(HYQ_EINVAL, "selector must be HYQ_SEL_PROXY or HYQ_SEL_COLMASS (got %d)",
                 s->selector);
@@ -164,8 +167,9 @@ int check_dcache(const hyq_dcache* c) {
       c->D != hyq::kHeadDim)
     return fail(HYQ_EINVAL, "cache geometry is invalid (B, Hq, Hkv, D)");
   if ((c->bits_kv != 8 && c->bits_kv != 4) ||
-      (c->kv_format != HYQ_FMT_INT && c->kv_format != HYQ_FMT_FP8) ||
-      (c->kv_format == HYQ_FMT_FP8 && c->bits_kv != 8))
+      (c->kv_format != HYQ_FMT_INT && c->kv_format != HYQ_FMT_FP8 && c->kv_format != HYQ_FMT_FP4) ||
+      (c->kv_format == HYQ_FMT_FP8 && c->bits_kv != 8) ||
+      (c->kv_format == HYQ_FMT_FP4 && c->bits_kv != 4))
     return fail(HYQ_EINVAL, "cache format is invalid (bits_kv %d, kv_format %d)", c->bits_kv,
                 c->kv_format);
   if (c->window < HYQ_DECODE_WS || c->n_vl < 0 || c->vl_rows != round_up64(c->n_vl) ||

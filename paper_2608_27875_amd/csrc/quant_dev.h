@@ -49,10 +49,28 @@ __device__ __forceinline__ int quant1_fp8(float x, float s) {
   return __builtin_amdgcn_cvt_pk_fp8_f32(y, 0.0f, 0, false) & 0xff;
 }
 
+// E2M1 code (0..15) of x / s (s > 0): the nearest of the magnitudes 0, 0.5,
+// 1, 1.5, 2, 3, 4, 6 (codes 0..7), a tie going to the even code, beyond 5
+// the largest; bit 3 is the sign of the quotient (so -0 gives 8).
+__device__ __forceinline__ int quant1_fp4(float x, float s) {
+  const float y = x / s;
+  const float a = fabsf(y);
+  const int c = (a > 0.25f) + (a >= 0.75f) + (a > 1.25f) + (a >= 1.75f) + (a > 2.5f) +
+                (a >= 3.5f) + (a > 5.0f);
+  return c | (int)((__float_as_uint(y) >> 31) << 3);
+}
+
 template <int FMT>
 __device__ __forceinline__ int quant_code(float x, float s, float c) {
   if (FMT == HYQ_FMT_FP8) return quant1_fp8(x, s);
+  if (FMT == HYQ_FMT_FP4) return quant1_fp4(x, s);
   return quant1(x, s, c);
+}
+
+// c_B of a code format and bit-width (Algorithm 2, Stage 2).
+template <int BITS, int FMT>
+constexpr float code_bound() {
+  return FMT == HYQ_FMT_FP8 ? 448.0f : FMT == HYQ_FMT_FP4 ? 6.0f : (BITS == 8 ? 127.0f : 7.0f);
 }
 
 }  // namespace hyq

@@ -104,8 +104,9 @@ quant_kv_kernel(const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
                 const int32_t* __restrict__ kq_pos, uint8_t* __restrict__ kc,
                 float* __restrict__ ks, uint8_t* __restrict__ vc, float* __restrict__ vs,
                 int L, int nQ, int n_kvblk) {
-  static_assert(FMT == HYQ_FMT_INT || BITS == 8, "FP8 codes are 8-bit");
-  constexpr float C = FMT == HYQ_FMT_FP8 ? 448.0f : (BITS == 8 ? 127.0f : 7.0f);
+  static_assert((FMT != HYQ_FMT_FP8 || BITS == 8) && (FMT != HYQ_FMT_FP4 || BITS == 4),
+                "FP8 codes are 8-bit, FP4 codes 4-bit");
+  constexpr float C = code_bound<BITS, FMT>();
   constexpr int kRow = BITS == 8 ? kHeadDim : kHeadDim / 2;   // bytes per K code row
   constexpr int vRow = BITS == 8 ? kBlock : kBlock / 2;        // bytes per V code row (one channel)
   __shared__ float red[kQuantThreads / 64];
@@ -212,7 +213,10 @@ void launch_quant_kv(int bits, int fmt, const uint16_t* K, const uint16_t* V,
                      hipStream_t st) {
   if (n_blocks <= 0) return;
   dim3 kg(n_blocks, BHkv);
-  if (fmt == HYQ_FMT_FP8)
+  if (fmt == HYQ_FMT_FP4)
+    quant_kv_kernel<4, HYQ_FMT_FP4><<<kg, kQuantThreads, 0, st>>>(
+        K, V, kq_pos, k_codes, k_scale, v_codes, v_scale, L, nQ, blk_stride);
+  else if (fmt == HYQ_FMT_FP8)
     quant_kv_kernel<8, HYQ_FMT_FP8><<<kg, kQuantThreads, 0, st>>>(
         K, V, kq_pos, k_codes, k_scale, v_codes, v_scale, L, nQ, blk_stride);
   else if (bits == 8)
@@ -231,7 +235,7 @@ hipError_t launch_quantize(const hyq_shape& s, const hyq_sizes& z, const uint16_
   const int BHkv = s.B * s.Hkv;
   launch_compact(idx, kq_pos, z.k, z.P, z.nQ, z.n_kvblk * kBlock, BHkv, st);
   dim3 qg(z.n_qblk, s.B * s.Hq);
-  if (s.kv_format == HYQ_FMT_FP8)
+  if (s.kv_format != HYQ_FMT_INT)   // E4M3 queries for both floating-point formats
     quant_q_kernel<HYQ_FMT_FP8><<<qg, kQuantThreads, 0, st>>>(Q, q_codes, q_scale, s.L, z.n_qblk);
   else
     quant_q_kernel<HYQ_FMT_INT><<<qg, kQuantThreads, 0, st>>>(Q, q_codes, q_scale, s.L, z.n_qblk);

@@ -22,8 +22,9 @@ def shape_of(cfg) -> hyq.Shape:
                      kv_format=cfg.get("fmt", hyq.FMT_INT))
 
 
-def fmt_name(shape: hyq.Shape) -> str:
-    return "fp8" if shape.kv_format == hyq.FMT_FP8 else "int"
+def fmt_name(shape) -> str:
+    """Oracle format name of a Shape or a decode cache struct."""
+    return {hyq.FMT_FP8: "fp8", hyq.FMT_FP4: "fp4"}.get(shape.kv_format, "int")
 
 
 def run_gpu(shape: hyq.Shape, d, out_dtype=0, keep_out_on_gpu=False, tensors=None):
@@ -56,6 +57,17 @@ def run_gpu(shape: hyq.Shape, d, out_dtype=0, keep_out_on_gpu=False, tensors=Non
     return g
 
 
+def unpack_codes4(raw: np.ndarray, fmt: int) -> np.ndarray:
+    """Packed 4-bit codes -> one code per element: two's-complement int4
+    values, or E2M1 codes 0..15 for FP4."""
+    if fmt == hyq.FMT_FP4:
+        out = np.empty(raw.shape[:-1] + (raw.shape[-1] * 2,), dtype=np.uint8)
+        out[..., 0::2] = raw & 0xF
+        out[..., 1::2] = raw >> 4
+        return out
+    return _nibbles(raw)
+
+
 def _nibbles(raw: np.ndarray) -> np.ndarray:
     """uint8 [..., n] of packed two's-complement nibbles -> int8 [..., 2n]
     (element 2i = low nibble of byte i)."""
@@ -78,7 +90,7 @@ def canonical(shape: hyq.Shape, g: dict) -> dict:
     slots = nb * 64
     kq = g["kq_pos"].reshape(B, Hkv, slots)
     assert np.all(kq[..., nQ:] == hyq.KQ_POS_PAD)
-    ctype = np.uint8 if shape.kv_format == hyq.FMT_FP8 else np.int8
+    ctype = np.int8 if shape.kv_format == hyq.FMT_INT else np.uint8
     out = dict(kq_pos=kq[..., :nQ],
                q_codes=g["q_codes"].view(ctype).reshape(B, Hq, L, D),
                q_scale=g["q_scale"].reshape(B, Hq, z["n_qblk"]),
@@ -88,8 +100,9 @@ def canonical(shape: hyq.Shape, g: dict) -> dict:
         kc = g["k_codes"].view(ctype).reshape(B, Hkv, slots, D)
         vc = g["v_codes"].view(ctype).reshape(B, Hkv, nb, D, 64)
     else:
-        kc = _nibbles(g["k_codes"].view(np.uint8).reshape(B, Hkv, slots, D // 2))
-        vc = _nibbles(g["v_codes"].view(np.uint8).reshape(B, Hkv, nb, D, 32))
+        kc = unpack_codes4(g["k_codes"].view(np.uint8).reshape(B, Hkv, slots, D // 2),
+                           shape.kv_format)
+        vc = unpack_codes4(g["v_codes"].view(np.uint8).reshape(B, Hkv, nb, D, 32), shape.kv_format)
     vc = vc.transpose(0, 1, 2, 4, 3).reshape(B, Hkv, slots, D)
     assert np.all(kc[:, :, nQ:] == 0) and np.all(vc[:, :, nQ:] == 0)
     out["k_codes"] = kc[:, :, :nQ]

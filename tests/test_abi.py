@@ -70,8 +70,9 @@ def test_sizes_match_oracle(lib, L, W, ppm, bits):
     (dict(block=0), hyq.HYQ_EINVAL),
     (dict(D=64), hyq.HYQ_EUNSUPPORTED), (dict(bits_kv=5), hyq.HYQ_EUNSUPPORTED),
     (dict(block=32), hyq.HYQ_EUNSUPPORTED), (dict(Hq=72, Hkv=8), hyq.HYQ_EUNSUPPORTED),
-    (dict(kv_format=2), hyq.HYQ_EINVAL), (dict(kv_format=-1), hyq.HYQ_EINVAL),
+    (dict(kv_format=3), hyq.HYQ_EINVAL), (dict(kv_format=-1), hyq.HYQ_EINVAL),
     (dict(kv_format=hyq.FMT_FP8, bits_kv=4), hyq.HYQ_EINVAL),
+    (dict(kv_format=hyq.FMT_FP4, bits_kv=8), hyq.HYQ_EINVAL),
     (dict(window_mode=2), hyq.HYQ_EINVAL), (dict(window_mode=-1), hyq.HYQ_EINVAL),
 ])
 def test_bad_shapes_rejected(lib, kw, code):
@@ -131,7 +132,7 @@ def test_shape_struct_layout_matches_header(tmp_path):
     src = ['#include <stdio.h>', '#include <stddef.h>', '#include "hyq.h"', 'int main(void) {',
            'printf("%zu\\n", sizeof(hyq_shape));']
     src += [f'printf("%zu\\n", offsetof(hyq_shape, {n}));' for n in names]
-    src += ['printf("%d %d %d %d\\n", HYQ_WIN_FIXED, HYQ_WIN_BAND, HYQ_FMT_INT, HYQ_FMT_FP8);',
+    src += ['printf("%d %d %d %d %d\\n", HYQ_WIN_FIXED, HYQ_WIN_BAND, HYQ_FMT_INT, HYQ_FMT_FP8, HYQ_FMT_FP4);',
             'return 0; }']
     c = tmp_path / "shape.c"
     c.write_text("\n".join(src))
@@ -141,7 +142,7 @@ def test_shape_struct_layout_matches_header(tmp_path):
     assert int(out[0]) == ctypes.sizeof(hyq._Shape)
     assert [int(v) for v in out[1:1 + len(names)]] == [getattr(hyq._Shape, n).offset for n in names]
     assert [int(v) for v in out[1 + len(names):]] == [hyq.WIN_FIXED, hyq.WIN_BAND, hyq.FMT_INT,
-                                                       hyq.FMT_FP8]
+                                                       hyq.FMT_FP8, hyq.FMT_FP4]
 
 
 def test_dcache_struct_layout_matches_header(tmp_path):

@@ -20,7 +20,7 @@ pytestmark = pytest.mark.gpu
 
 
 def _fmt(shape):
-    return "fp8" if shape.kv_format == hyq.FMT_FP8 else "int"
+    return gc.fmt_name(shape)
 
 
 def _rows(rng, B, H, D=128):
@@ -36,13 +36,14 @@ def _gpu_view(cache: hyq.DecodeCache) -> dict:
     nfp = c.vl_rows + c.ring_rows
     fk = cache.bufs["fp_k"].view(__import__("torch").int16).cpu().numpy().view(np.uint16)
     fv = cache.bufs["fp_v"].view(__import__("torch").int16).cpu().numpy().view(np.uint16)
-    ctype = np.uint8 if c.kv_format == hyq.FMT_FP8 else np.int8
+    ctype = np.int8 if c.kv_format == hyq.FMT_INT else np.uint8
     if c.bits_kv == 8:
         kc = b["k_codes"][:BH * cap * 64 * D].view(ctype).reshape(BH, cap * 64, D)
         vc = b["v_codes"][:BH * cap * D * 64].view(ctype).reshape(BH, cap, D, 64)
     else:
-        kc = gc._nibbles(b["k_codes"][:BH * cap * 64 * D // 2].reshape(BH, cap * 64, D // 2))
-        vc = gc._nibbles(b["v_codes"][:BH * cap * D * 32].reshape(BH, cap, D, 32))
+        kc = gc.unpack_codes4(b["k_codes"][:BH * cap * 64 * D // 2].reshape(BH, cap * 64, D // 2),
+                              c.kv_format)
+        vc = gc.unpack_codes4(b["v_codes"][:BH * cap * D * 32].reshape(BH, cap, D, 32), c.kv_format)
     vc = vc.transpose(0, 1, 3, 2).reshape(BH, cap * 64, D)
     return dict(kc=kc, vc=vc, ks=b["k_scale"][:BH * cap].reshape(BH, cap),
                 vs=b["v_scale"][:BH * cap].reshape(BH, cap),
@@ -133,6 +134,9 @@ SMALL = [
     ("int8_budget0", 1, 4, 1, 450, 96, 0, 8, hyq.FMT_INT),
     ("int4_all_vertical", 1, 4, 1, 200, 64, 1000000, 4, hyq.FMT_INT),
     ("fp8_window_only", 1, 4, 1, 64, 64, 50000, 8, hyq.FMT_FP8),
+    ("fp4_g4", 1, 8, 2, 700, 64, 30000, 4, hyq.FMT_FP4),
+    ("fp4_b2_g5_w100", 2, 10, 2, 517, 100, 20000, 4, hyq.FMT_FP4),
+    ("fp4_g8_w128", 1, 16, 2, 1100, 128, 50000, 4, hyq.FMT_FP4),
 ]
 
 
@@ -201,11 +205,13 @@ def test_decode_cache_full_is_an_error():
 
 
 @pytest.mark.timeout(600)
-def test_decode_32k_k4v4_top5_w128():
+@pytest.mark.parametrize("fmt", [hyq.FMT_INT, hyq.FMT_FP4], ids=["int4", "fp4"])
+def test_decode_32k_k4v4_top5_w128(fmt):
     """The paper's decode-latency workload: batch 1, 32 query / 8 KV heads,
     d 128, 32k-token prefix, K4V4, top-5% vertical lines, window 128."""
     N, W = 32768, 128
-    shape = hyq.Shape(B=1, Hq=32, Hkv=8, L=N, window=W, budget_ppm=50000, bits_kv=4)
+    shape = hyq.Shape(B=1, Hq=32, Hkv=8, L=N, window=W, budget_ppm=50000, bits_kv=4,
+                      kv_format=fmt)
     print("generating", flush=True)
     d = gen.generate(0, 7, B=1, Hq=32, Hkv=8, L=N, D=128, W=W, plant=0.05,
                      outliers=(3, 47, 85, 122))
