@@ -134,7 +134,7 @@ def decode_bytes(c, B):
 
 
 def decode_record(B, layers, steps, budget_ppm=50000, bits=4, N=32768, W=128, Hq=32, Hkv=8,
-                  seed=0, label=None, probe=False):
+                  seed=0, label=None, probe=False, fmt=0):
     """Freeze `layers` synthetic layers, then time hyq_decode_attn over all of
     them (one decode token of a `layers`-layer model)."""
     import numpy as np
@@ -143,7 +143,8 @@ def decode_record(B, layers, steps, budget_ppm=50000, bits=4, N=32768, W=128, Hq
     import paper_2608_27875_amd as hyq
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
-    shape = hyq.Shape(B=B, Hq=Hq, Hkv=Hkv, L=N, window=W, budget_ppm=budget_ppm, bits_kv=bits)
+    shape = hyq.Shape(B=B, Hq=Hq, Hkv=Hkv, L=N, window=W, budget_ppm=budget_ppm, bits_kv=bits,
+                      kv_format=fmt)
     gen_ = torch.Generator(device=dev)
     gen_.manual_seed(seed)
     caches, qs, outs = [], [], []
@@ -218,7 +219,8 @@ def decode_record(B, layers, steps, budget_ppm=50000, bits=4, N=32768, W=128, Hq
     us_layer = ms * 1e3 / layers
     nbytes = decode_bytes(caches[0].c, B)
     gbs = nbytes / (us_layer * 1e-6) / 1e9
-    workload = label or f"decode_gqa{Hq}q{Hkv}kv_d128_B{B}_N{N}_W{W}_r{budget_ppm}ppm_kv{bits}bit"
+    workload = label or (f"decode_gqa{Hq}q{Hkv}kv_d128_B{B}_N{N}_W{W}_r{budget_ppm}ppm_kv{bits}bit" +
+                         ("_fp4" if fmt == hyq.FMT_FP4 else ""))
     rec = {"workload": workload,
            "layers": layers, "us_per_layer": round(us_layer, 3),
            "timing": "hip graph of the layer loop" if graph_ok else "eager launches",
@@ -235,8 +237,9 @@ def decode_record(B, layers, steps, budget_ppm=50000, bits=4, N=32768, W=128, Hq
 
 
 def decode_section(layers, steps):
-    """The decode measurements: K4V4 hybrid at batch 1 and 16, and the
-    all-bf16 comparison (every prefix token a vertical line) at batch 1."""
+    """The decode measurements: K4V4 hybrid at batch 1 and 16, the same with
+    FP4 (E2M1) codes at batch 1, and the all-bf16 comparison (every prefix
+    token a vertical line) at batch 1."""
     r1 = decode_record(1, layers, steps)
     bf = decode_record(1, layers, steps, budget_ppm=1000000, bits=8,
                        label="decode_gqa32q8kv_d128_B1_N32768_all_bf16")
@@ -244,6 +247,10 @@ def decode_section(layers, steps):
                               "bytes_per_layer": bf["bytes_per_layer"],
                               "achieved_gbs": bf["roofline"]["achieved"],
                               "speedup_of_hybrid": round(bf["us_per_layer"] / r1["us_per_layer"], 3)}
+    import paper_2608_27875_amd as hyq
+    f4 = decode_record(1, layers, steps, fmt=hyq.FMT_FP4)
+    r1["fp4_same_length"] = {k: f4[k] for k in ("workload", "us_per_layer", "bytes_per_layer")}
+    r1["fp4_same_length"]["achieved_gbs"] = f4["roofline"]["achieved"]
     r16 = decode_record(16, max(2, layers // 9), steps)
     r1["batch16"] = {k: r16[k] for k in ("workload", "layers", "us_per_layer", "bytes_per_layer",
                                          "roofline")}
@@ -415,6 +422,47 @@ def main():
                   "speedup_of_hybrid": round(ms16 / float(np.median(att)), 3)}
         del b16
 
+    def quant_attn_ms(sx, reps=10):
+        """Median of quantize + attention (timed around the attention only)
+        for another bit-width / format on the same inputs and selection."""
+        bx = hyq.alloc_buffers(sx, dev, out_dtype)
+        hyq.hyq_select_vertical(sx, Q, K, bx["idx"], None, bx["ws"], stream)
+
+        def stepx(e=None):
+            hyq.hyq_quantize(sx, Q, K, V, bx["idx"], bx["q_codes"], bx["q_scale"],
+                             bx["k_codes"], bx["k_scale"], bx["v_codes"], bx["v_scale"],
+                             bx["kq_pos"], stream)
+            if e:
+                e[0].record(stream)
+            hyq.hyq_attn_prefill(sx, Q, K, V, bx["idx"], bx["q_codes"], bx["q_scale"],
+                                 bx["k_codes"], bx["k_scale"], bx["v_codes"], bx["v_scale"],
+                                 bx["kq_pos"], scale, bx["out"], out_dtype, stream)
+            if e:
+                e[1].record(stream)
+        for _ in range(2):
+            stepx()
+        torch.cuda.synchronize()
+        ex = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(reps)]
+        for e in ex:
+            stepx(e)
+        torch.cuda.synchronize()
+        del bx
+        return float(np.median([e[0].elapsed_time(e[1]) for e in ex]))
+
+    # the same inputs with 4-bit K/V codes: int4 (int8 queries, int8 MFMA)
+    # and FP4 E2M1 (E4M3 queries, E2M1 keys as the scaled MFMA's 4-bit operand)
+    four_bit = None
+    if not args.no_fp8 and shape.bits_kv == 8 and fmt == hyq.FMT_INT:
+        print("[bench] 4-bit codes (int4, fp4)", file=sys.stderr, flush=True)
+        fl = causal_flops(shape.B, shape.Hq, shape.L, shape.D)
+        four_bit = {}
+        for name, fx in (("int4", hyq.FMT_INT), ("fp4", hyq.FMT_FP4)):
+            msx = quant_attn_ms(dataclasses.replace(shape, bits_kv=4, kv_format=fx))
+            tfx = fl / (msx * 1e-3) / 1e12
+            four_bit[name] = {"attention_ms_median": round(msx, 4), "tflops": round(tfx, 2),
+                              "frac_int8_fp8_peak": round(tfx / INT8_PEAK_TOPS, 4)}
+
     # the same inputs with FP8 (E4M3) codes: quantize + attention
     fp8 = None
     if not args.no_fp8 and shape.bits_kv == 8 and fmt == hyq.FMT_INT:
@@ -564,6 +612,7 @@ def main():
                       "quantize": round(float(np.median(qnt)), 4)},
         "bits16_same_inputs": bits16,
         "fp8_same_inputs": fp8,
+        "four_bit_same_inputs": four_bit,
         "band_window_same_inputs": band,
         "colmass_selector_same_inputs": colmass,
         "attention_tflops": round(attn_tflops, 2),
