@@ -96,7 +96,8 @@ def cpu_baseline(d, cfg, flops_total, budget_s):
     idx, _ = orc.select_vertical(d["Q"], d["K"], cfg["Hkv"], W, cfg["budget_ppm"])
     t_sel = time.perf_counter() - t0
     t0 = time.perf_counter()
-    qz = orc.quantize(d["Q"], d["K"], d["V"], idx, W, cfg["bits"])
+    qz = orc.quantize(d["Q"], d["K"], d["V"], idx, W, cfg["bits"],
+                      fmt=cfg.get("fmt_name", "int") if cfg["bits"] != 16 else "int")
     t_quant = time.perf_counter() - t0
     heads = [(0, h) for h in range(0, Hq, max(1, Hq // 4))][:4]
     rng = np.random.default_rng(0)
@@ -274,8 +275,9 @@ def main():
                          "is one GPU's share of config 3 under 8-way head sharding")
     ap.add_argument("--no-bits16", action="store_true",
                     help="skip the full-precision (bits 16) attention of the same inputs")
-    ap.add_argument("--fmt", choices=("int", "fp8"), default="int",
-                    help="code format of the quantized path (fp8 = OCP E4M3, 8-bit only)")
+    ap.add_argument("--fmt", choices=("int", "fp8", "fp4"), default="int",
+                    help="code format of the quantized path (fp8 = OCP E4M3, 8-bit only; "
+                         "fp4 = OCP E2M1 K/V with E4M3 queries, sets bits 4)")
     ap.add_argument("--no-fp8", action="store_true",
                     help="skip the FP8-code run of the same inputs")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode measurement")
@@ -335,7 +337,10 @@ def main():
         cfg["Hq"], cfg["Hkv"] = args.hq, hkv
     Q, K, V = t(np.ascontiguousarray(d["Q"])), t(np.ascontiguousarray(d["K"])), \
         t(np.ascontiguousarray(d["V"]))
-    fmt = hyq.FMT_FP8 if args.fmt == "fp8" else hyq.FMT_INT
+    fmt = {"fp8": hyq.FMT_FP8, "fp4": hyq.FMT_FP4}.get(args.fmt, hyq.FMT_INT)
+    if fmt == hyq.FMT_FP4:
+        cfg["bits"] = 4
+    cfg["fmt_name"] = args.fmt
     shape = hyq.Shape(B=cfg["B"], Hq=cfg["Hq"], Hkv=cfg["Hkv"], L=cfg["L"], window=cfg["W"],
                       budget_ppm=cfg["budget_ppm"], bits_kv=cfg["bits"], kv_format=fmt)
     out_dtype = 1 if args.out_bf16 else 0
@@ -573,7 +578,8 @@ def main():
                    z["q_codes_bytes"] + z["k_codes_bytes"] + z["v_codes_bytes"] +
                    z["q_scale_bytes"] + 2 * z["kv_scale_bytes"] + z["kq_pos_bytes"] + z["idx_bytes"])
     workload = (f"gqa{shape.Hq}q{shape.Hkv}kv_d{shape.D}_B{shape.B}_L{shape.L}_W{shape.window}"
-                f"_r{shape.budget_ppm}ppm_kv{shape.bits_kv}bit" + ("_fp8" if fmt == hyq.FMT_FP8 else ""))
+                f"_r{shape.budget_ppm}ppm_kv{shape.bits_kv}bit" +
+                {hyq.FMT_FP8: "_fp8", hyq.FMT_FP4: "_fp4"}.get(fmt, ""))
     traffic = load_traffic(workload)
     planted = d["planted"]
     idx = bufs["idx"].cpu().numpy()
@@ -595,7 +601,8 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": ("bf16" if shape.bits_kv == 16 else
-                  "e4m3+f16" if fmt == hyq.FMT_FP8 else "i8+f16"),
+                  "e4m3+f16" if fmt == hyq.FMT_FP8 else
+                  "e2m1xe4m3+f16" if fmt == hyq.FMT_FP4 else "i8+f16"),
         "data": "synthetic (seeded Gaussian Q/K/V, planted vertical lines, x10 outlier K channels)",
         "config": {"workload": workload, "B": shape.B, "Hq": shape.Hq, "Hkv": shape.Hkv,
                    "L": shape.L, "D": shape.D, "window": shape.window,
