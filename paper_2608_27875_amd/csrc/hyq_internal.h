@@ -18,7 +18,6 @@ hipError_t launch_select(const hyq_shape& s, const hyq_sizes& z, const uint16_t*
 
 // Column-mass scores (eq. vl_score) into scores[B][Hkv][P]; cm_ws holds
 // colmass_ws_bytes(s) bytes of scratch.
-constexpr int kColmassSplits = 4;   // key-axis splits of the normalizer pass
 size_t colmass_ws_bytes(const hyq_shape& s);
 hipError_t launch_colmass_scores(const hyq_shape& s, const hyq_sizes& z, const uint16_t* Q,
                                  const uint16_t* K, float* scores, float* cm_ws, hipStream_t st);
