@@ -103,42 +103,14 @@ __device__ __forceinline__ uint32_t order_key(float f) {
 constexpr int kTopkThreads = 1024;
 constexpr int kTopkWaves = kTopkThreads / 64;
 
-// Exclusive prefix sum over the workgroup (1024 threads); also returns the total.
-__device__ int block_exclusive_scan(int v, int* sh, int& total) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) sh[w] = x;
-  __syncthreads();
-  if (w == 0) {
-    int t = lane < kTopkWaves ? sh[lane] : 0;
-#pragma unroll
-    for (int o = 1; o < kTopkWaves; o <<= 1) {
-      const int y = __shfl_up(t, o, 64);
-      if (lane >= o) t += y;
-    }
-    if (lane < kTopkWaves) sh[kTopkWaves + lane] = t;
-  }
-  __syncthreads();
-  total = sh[kTopkWaves + kTopkWaves - 1];
-  const int before = (w > 0 ? sh[kTopkWaves + w - 1] : 0) + x - v;
-  __syncthreads();
-  return before;
-}
-
 // One workgroup per (b, j).  Radix select over the 32-bit order keys, 8 bits
 // per pass (per-wave LDS histograms), finds the k-th largest key T and how
 // many keys equal to T are taken (the lowest positions).  Then an ordered
-// compaction writes the chosen positions ascending: thread i owns a
-// contiguous run of positions; two block scans give each run's offsets.
+// compaction writes the chosen positions ascending (below).
 __global__ void __launch_bounds__(kTopkThreads)
 topk_kernel(const float* __restrict__ S, int32_t* __restrict__ idx, int P, int k) {
   __shared__ uint32_t hist[kTopkWaves][256];
-  __shared__ int scan_sh[2 * kTopkWaves];
+  __shared__ int w_gt[kTopkWaves], w_eq[kTopkWaves];
   __shared__ uint32_t sh_digit;
   __shared__ int sh_remaining;
   const int bj = blockIdx.x;
@@ -196,27 +168,49 @@ topk_kernel(const float* __restrict__ S, int32_t* __restrict__ idx, int P, int k
   const uint32_t T = prefix;
   const int need_eq = remaining;  // keys equal to T to take, lowest positions first
 
-  const int run = (P + kTopkThreads - 1) / kTopkThreads;
-  const int p0 = min(P, threadIdx.x * run), p1 = min(P, p0 + run);
-  int gt = 0, eq = 0;
-  for (int p = p0; p < p1; ++p) {
-    const uint32_t u = order_key(s[p]);
-    gt += u > T;
-    eq += u == T;
+  // Ordered compaction: wave w owns positions [w*R, (w+1)*R) and reads them
+  // 64 at a time (coalesced); a first sweep counts its keys above and equal to
+  // T, the wave totals give each wave its output offset and its share of the
+  // keys equal to T, a second sweep writes the positions in order.
+  const int R = ((P + kTopkWaves - 1) / kTopkWaves + 63) & ~63;
+  const int q0 = min(P, w * R), q1 = min(P, q0 + R);
+  int gtc = 0, eqc = 0;   // wave-uniform
+  for (int b = q0; b < q1; b += 64) {
+    const int p = b + lane;
+    const uint32_t u = p < q1 ? order_key(s[p]) : 0u;
+    gtc += (int)__popcll(__ballot(p < q1 && u > T));
+    eqc += (int)__popcll(__ballot(p < q1 && u == T));
   }
-  int tot;
-  const int eq_before = block_exclusive_scan(eq, scan_sh, tot);
-  const int take_eq = max(0, min(eq, need_eq - eq_before));
-  const int out0 = block_exclusive_scan(gt + take_eq, scan_sh, tot);
+  if (lane == 0) {
+    w_gt[w] = gtc;
+    w_eq[w] = eqc;
+  }
+  __syncthreads();
+  int o = 0, eq_before = 0;
+  for (int v = 0; v < w; ++v) {
+    o += w_gt[v] + max(0, min(w_eq[v], need_eq - eq_before));
+    eq_before += w_eq[v];
+  }
+  const int take_eq = max(0, min(eqc, need_eq - eq_before));
   int32_t* out = idx + (size_t)bj * k;
-  int o = out0, te = 0;
-  for (int p = p0; p < p1; ++p) {
-    const uint32_t u = order_key(s[p]);
-    if (u > T || (u == T && te < take_eq)) {
-      if (o < k) out[o] = p;   // never more than k (guards a malformed threshold)
-      ++o;
-      te += (u == T);
+  int eq_seen = 0;
+  for (int b = q0; b < q1; b += 64) {
+    const int p = b + lane;
+    const bool in = p < q1;
+    const uint32_t u = in ? order_key(s[p]) : 0u;
+    const bool is_eq = in && u == T;
+    const uint64_t meq = __ballot(is_eq);
+    const int eq_rank = eq_seen + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(meq >> 32),
+                                      __builtin_amdgcn_mbcnt_lo((uint32_t)meq, 0u));
+    const bool sel = in && (u > T || (is_eq && eq_rank < take_eq));
+    const uint64_t msel = __ballot(sel);
+    if (sel) {
+      const int pos = o + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(msel >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)msel, 0u));
+      if (pos < k) out[pos] = p;   // never more than k (guards a malformed threshold)
     }
+    o += (int)__popcll(msel);
+    eq_seen += (int)__popcll(meq);
   }
 }
 
