@@ -88,7 +88,8 @@ typedef struct hyq_shape {
   int32_t B, Hq, Hkv, L, D;  /* batch, query heads, KV heads, sequence, head dim      */
   int32_t window;            /* W >= 0: full-precision window = last W keys          */
   int32_t budget_ppm;        /* vertical ratio r in parts per million, 0..1000000    */
-  int32_t bits_kv;           /* 16 (no quantization), 8 (int8) or 4 (packed int4)   */
+  int32_t bits_kv;           /* 16 (no quantization), 8 (int8 / E4M3) or 4 (packed
+                                int4 / E2M1), see kv_format                          */
   int32_t block;             /* quantization block in tokens (64)                   */
   int32_t kv_format;         /* HYQ_FMT_INT, HYQ_FMT_FP8 (bits 8) or HYQ_FMT_FP4 (bits
                                 4); ignored when bits = 16                          */
@@ -152,12 +153,14 @@ HYQ_API int hyq_select_vertical(const hyq_shape* shape, const void* Q, const voi
  *   K/V blocks:      compacted rows [c*64, c*64+64) (K and V at kq_pos),
  *                    ragged last block; padding rows get code 0.
  *   scale s = fl32(max|x| / c), code = clamp(rint(fl32(x / s)), -c, c),
- *   c = 127 for Q and 8-bit K/V, c = 7 for 4-bit K/V; s = 0 gives codes 0.
+ *   c = 127 for Q and 8-bit K/V, c = 7 for 4-bit K/V; s = 0 gives codes 0
+ *   (HYQ_FMT_INT; the floating-point formats round as described at
+ *   HYQ_FMT_FP8 and HYQ_FMT_FP4, Q then in E4M3 with c = 448).
  * Layouts (all outputs written in full, padding included):
  *   q_codes int8 [B][Hq][L][D];           q_scale float [B][Hq][n_qblk]
- *   k_codes [B][Hkv][n_kvblk*64][row]:    8-bit: int8 per channel;
+ *   k_codes [B][Hkv][n_kvblk*64][row]:    8-bit: one code byte per channel;
  *            4-bit: byte i = channel 2i (low nibble) | channel 2i+1 (high
- *            nibble), two's-complement nibbles;
+ *            nibble), two's-complement int4 or E2M1 nibbles;
  *   v_codes [B][Hkv][n_kvblk][D][64*bits/8]: each block stored channel-major
  *            (transposed): row d lists the block's 64 keys; 4-bit: byte i =
  *            key 2i (low nibble) | key 2i+1 (high nibble);
@@ -187,7 +190,8 @@ HYQ_API int hyq_quantize(const hyq_shape* shape, const void* Q, const void* K, c
  * The quantization buffers (q_codes ... kq_pos) are the outputs of
  * hyq_quantize for the same shape; they are not read when bits_kv = 16.
  * Precision: quantized logits are exact int32 dot products scaled in
- * float32; full-precision logits are bf16 x bf16 products accumulated in
+ * float32 (int codes) or the float32 results of the E4M3 / E2M1 x E4M3
+ * MFMA; full-precision logits are bf16 x bf16 products accumulated in
  * float32; softmax weights enter the P.V products as f16 (quantized keys,
  * against exact f16 codes) or as a high + low pair of bf16 (full-precision
  * keys, against bf16 V); all accumulation is float32.
