@@ -12,7 +12,7 @@
 //   colmass_lse_kernel   per query row, log2-sum-exp over its keys, split
 //                        over the key axis into partials;
 //   colmass_merge_kernel the partials of each row merged;
-//   colmass_sum_kernel   per 64 prefix keys, the probabilities of every
+//   colmass_sum_kernel   per prefix key, the probabilities of every
 //                        considered row summed (prefix keys precede every
 //                        tail row, so no mask).
 // Both passes are bf16 MFMA products with keys as rows (S^T = K Q^T), the
