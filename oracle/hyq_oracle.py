@@ -675,15 +675,18 @@ DECODE_WS = 64
 
 
 def freeze(Qb, Kb, Vb, Hkv: int, W: int, budget_ppm: int, bits: int, block: int = 64,
-           fmt: str = "int", selector: str = "proxy"):
+           fmt: str = "int", selector: str = "proxy", staging: int = DECODE_WS):
     """Algorithm 4 on a prefill of N tokens (bf16 inputs).  Returns the hybrid
     cache as a dict of numpy arrays (per (b, j) lists where sizes can grow):
     quantized prefix (kq_pos, k/v codes and scales per block), vertical-line
-    rows, window rows, an empty staging buffer."""
+    rows, window rows, an empty staging buffer of capacity ``staging`` (W_s,
+    a multiple of the block)."""
     if bits == 16:
         raise ValueError("freeze needs a quantized format (bits 8 or 4)")
     B, Hq, N, D = Qb.shape
-    if W < DECODE_WS or N < W:
+    if staging < block or staging % block:
+        raise ValueError("the staging capacity is a positive multiple of the block")
+    if W < staging or N < W:
         raise ValueError("decode needs W >= Ws (merges move Ws window tokens) and N >= W")
     if selector == "colmass":
         idx, _ = select_vertical_colmass(Qb, Kb, Hkv, W, budget_ppm)
@@ -693,7 +696,8 @@ def freeze(Qb, Kb, Vb, Hkv: int, W: int, budget_ppm: int, bits: int, block: int 
     P = max(0, N - W)
     nq = qz["kq_pos"].shape[2]
     nb = -(-nq // block)
-    cache = dict(B=B, Hq=Hq, Hkv=Hkv, D=D, W=W, bits=bits, fmt=fmt, block=block, t=N, idx=idx)
+    cache = dict(B=B, Hq=Hq, Hkv=Hkv, D=D, W=W, bits=bits, fmt=fmt, block=block, t=N, idx=idx,
+                 Ws=staging)
     kc, vc, ks, vs, pos = [], [], [], [], []
     for b in range(B):
         for j in range(Hkv):
@@ -727,21 +731,23 @@ def _quantize_block(rows_f32: np.ndarray, cache):
 
 
 def decode_merge(cache):
-    """Staging full: quantize the Ws oldest window tokens into one new block
-    of the quantized prefix; the staging tokens join the window."""
-    Ws = DECODE_WS
+    """Staging full: quantize the Ws oldest window tokens into Ws / block new
+    blocks of the quantized prefix (oldest first, each with its own scale,
+    as Freeze quantizes); the staging tokens join the window."""
+    Ws, G = cache["Ws"], cache["block"]
     for bj in range(cache["B"] * cache["Hkv"]):
         if cache["W"] < Ws or len(cache["st_k"][bj]) != Ws:
             raise ValueError("merge needs W >= Ws and a full staging buffer")
-        ek = bf16_to_f32(np.stack(cache["win_k"][bj][:Ws]))
-        ev = bf16_to_f32(np.stack(cache["win_v"][bj][:Ws]))
-        kcode, ksc = _quantize_block(ek, cache)
-        vcode, vsc = _quantize_block(ev, cache)
-        cache["k_blocks"][bj].append(kcode)
-        cache["v_blocks"][bj].append(vcode)
-        cache["k_scales"][bj].append(ksc[0])
-        cache["v_scales"][bj].append(vsc[0])
-        cache["q_pos"][bj].append(np.array(cache["win_pos"][bj][:Ws], np.int32))
+        for i in range(0, Ws, G):
+            ek = bf16_to_f32(np.stack(cache["win_k"][bj][i:i + G]))
+            ev = bf16_to_f32(np.stack(cache["win_v"][bj][i:i + G]))
+            kcode, ksc = _quantize_block(ek, cache)
+            vcode, vsc = _quantize_block(ev, cache)
+            cache["k_blocks"][bj].append(kcode)
+            cache["v_blocks"][bj].append(vcode)
+            cache["k_scales"][bj].append(ksc[0])
+            cache["v_scales"][bj].append(vsc[0])
+            cache["q_pos"][bj].append(np.array(cache["win_pos"][bj][i:i + G], np.int32))
         for name in ("k", "v", "pos"):
             w, st = cache["win_" + name], cache["st_" + name]
             w[bj] = w[bj][Ws:] + st[bj]
@@ -751,7 +757,7 @@ def decode_merge(cache):
 def decode_append(cache, k_new, v_new):
     """One new token's key and value rows (bf16 bits [B, Hkv, D]) enter the
     staging buffer (merging it first if it is full)."""
-    if len(cache["st_k"][0]) == DECODE_WS:
+    if len(cache["st_k"][0]) == cache["Ws"]:
         decode_merge(cache)
     t = cache["t"]
     for b in range(cache["B"]):

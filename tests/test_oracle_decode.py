@@ -169,3 +169,42 @@ def test_freeze_domain():
         orc.freeze(d["Q"], d["K"], d["V"], 1, 128, 10000, 8)       # N < W
     with pytest.raises(ValueError):
         orc.freeze(d["Q"], d["K"], d["V"], 1, 64, 10000, 16)       # nothing quantized
+
+
+@pytest.mark.parametrize("fmt,bits", [("int", 8), ("fp4", 4)])
+def test_merge_with_a_two_block_staging_buffer(fmt, bits):
+    """Staging capacity 128 (the memory-overhead example of the paper): the
+    129th token merges the 128 oldest window tokens into two blocks, each
+    quantized on its own (exact rationals), oldest first."""
+    N, W, D = 300, 128, 8
+    d = _prefill(11, 1, 2, 1, N, D, W)
+    c = orc.freeze(d["Q"], d["K"], d["V"], 1, W, 30000, bits, fmt=fmt, staging=128)
+    nb0 = len(c["k_blocks"][0])
+    oldest_k = np.stack(c["win_k"][0][:128])
+    oldest_pos = c["win_pos"][0][:128]
+    rng = np.random.default_rng(12)
+    added = []
+    for step in range(129):
+        kn, vn = _new_rows(rng, 1, 1, D), _new_rows(rng, 1, 1, D)
+        orc.decode_append(c, kn, vn)
+        added.append(kn[0, 0])
+        if step < 128:
+            assert len(c["k_blocks"][0]) == nb0           # no merge before the 129th token
+    assert len(c["k_blocks"][0]) == nb0 + 2
+    assert len(c["win_k"][0]) == W and len(c["st_k"][0]) == 1
+    assert sorted(_all_positions(c, 0).tolist()) == list(range(N + 129))
+    for i in range(2):
+        x = gen.bf16_bits_to_f32(oldest_k[64 * i:64 * (i + 1)]).ravel()
+        codes, s = brute.quant_block_fp4_exact(x) if fmt == "fp4" else \
+            brute.quant_block_exact(x, orc.code_bound(bits))
+        assert np.ravel(c["k_blocks"][0][nb0 + i]).tolist() == codes
+        assert float(c["k_scales"][0][nb0 + i]) == s
+        assert list(c["q_pos"][0][nb0 + i]) == oldest_pos[64 * i:64 * (i + 1)]
+    np.testing.assert_array_equal(np.stack(c["win_k"][0]), np.stack(added[:128]))
+
+
+def test_staging_capacity_domain():
+    d = _prefill(13, 1, 2, 1, 300, 8, 128)
+    for bad in (0, 32, 100, 192):                           # not a block multiple, or > W
+        with pytest.raises(ValueError):
+            orc.freeze(d["Q"], d["K"], d["V"], 1, 128, 10000, 8, staging=bad)
