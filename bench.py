@@ -135,7 +135,7 @@ def decode_bytes(c, B):
 
 
 def decode_record(B, layers, steps, budget_ppm=50000, bits=4, N=32768, W=128, Hq=32, Hkv=8,
-                  seed=0, label=None, probe=False, fmt=0):
+                  seed=0, label=None, probe=False, fmt=0, staging=128):
     """Freeze `layers` synthetic layers, then time hyq_decode_attn over all of
     them (one decode token of a `layers`-layer model)."""
     import numpy as np
@@ -145,7 +145,7 @@ def decode_record(B, layers, steps, budget_ppm=50000, bits=4, N=32768, W=128, Hq
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
     shape = hyq.Shape(B=B, Hq=Hq, Hkv=Hkv, L=N, window=W, budget_ppm=budget_ppm, bits_kv=bits,
-                      kv_format=fmt)
+                      kv_format=fmt, staging=staging)
     gen_ = torch.Generator(device=dev)
     gen_.manual_seed(seed)
     caches, qs, outs = [], [], []
@@ -220,8 +220,8 @@ def decode_record(B, layers, steps, budget_ppm=50000, bits=4, N=32768, W=128, Hq
     us_layer = ms * 1e3 / layers
     nbytes = decode_bytes(caches[0].c, B)
     gbs = nbytes / (us_layer * 1e-6) / 1e9
-    workload = label or (f"decode_gqa{Hq}q{Hkv}kv_d128_B{B}_N{N}_W{W}_r{budget_ppm}ppm_kv{bits}bit" +
-                         ("_fp4" if fmt == hyq.FMT_FP4 else ""))
+    workload = label or (f"decode_gqa{Hq}q{Hkv}kv_d128_B{B}_N{N}_W{W}_Ws{staging}_r{budget_ppm}ppm"
+                         f"_kv{bits}bit" + ("_fp4" if fmt == hyq.FMT_FP4 else ""))
     rec = {"workload": workload,
            "layers": layers, "us_per_layer": round(us_layer, 3),
            "timing": "hip graph of the layer loop" if graph_ok else "eager launches",

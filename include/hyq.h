@@ -95,6 +95,8 @@ typedef struct hyq_shape {
                                 4); ignored when bits = 16                          */
   int32_t window_mode;       /* HYQ_WIN_FIXED or HYQ_WIN_BAND                       */
   int32_t selector;          /* HYQ_SEL_PROXY or HYQ_SEL_COLMASS                    */
+  int32_t staging;           /* decode only: staging capacity W_s in tokens, 0 for
+                                HYQ_DECODE_WS, else a multiple of 64 <= window      */
 } hyq_shape;
 
 typedef struct hyq_sizes {
@@ -213,17 +215,19 @@ HYQ_API int hyq_attn_prefill(const hyq_shape* shape, const void* Q, const void* 
  *   - the other non-window tokens [0, N-W) minus the vertical lines:
  *     per-block quantized exactly as hyq_quantize quantizes K_Q and V_Q;
  *   - the last W tokens (the window): kept in bf16;
- *   - an empty staging buffer of HYQ_DECODE_WS tokens, kept in bf16.
+ *   - an empty staging buffer of W_s tokens (shape.staging, default
+ *     HYQ_DECODE_WS), kept in bf16.
  * Each decode step appends one token.  When it arrives with the staging
- * buffer full, the HYQ_DECODE_WS oldest window tokens are first quantized
- * into one new block of the quantized prefix (same formula, c_B and format)
- * and the staged tokens join the window, which stays W tokens long.
+ * buffer full, the W_s oldest window tokens are first quantized into W_s/64
+ * new blocks of the quantized prefix (same formula, c_B and format, 64
+ * tokens per block, oldest first) and the staged tokens join the window,
+ * which stays W tokens long.
  * Decode attention of one query row per (b, h) is one softmax over every
  * cached key (no mask): quantized keys enter as scale * code, all other
  * keys as their bf16 values; the query is used in full precision.
  *
  * Memory: the window and the staging buffer share one ring of
- * ring_rows = roundup(W, 64) + 64 bf16 rows per KV head (window = the W
+ * ring_rows = roundup(W, 64) + W_s bf16 rows per KV head (window = the W
  * oldest valid rows from ring_head on, staging = the rest), so a merge
  * moves no full-precision data.  Vertical-line rows and the ring are stored
  * together: fp_k row i < vl_rows is vertical line i (rows >= n_vl are zero
@@ -233,7 +237,7 @@ HYQ_API int hyq_attn_prefill(const hyq_shape* shape, const void* Q, const void* 
  * hyq_decode_append advances on the host.
  * ==================================================================== */
 
-#define HYQ_DECODE_WS 64   /* staging buffer capacity W_s (tokens)            */
+#define HYQ_DECODE_WS 64   /* default staging buffer capacity W_s (tokens)    */
 
 typedef struct hyq_dcache {
   /* geometry, set by hyq_dcache_init */
@@ -243,14 +247,14 @@ typedef struct hyq_dcache {
   int32_t kv_format;     /* HYQ_FMT_INT, HYQ_FMT_FP8 (bits 8) or HYQ_FMT_FP4 (bits 4)*/
   int32_t n_vl;          /* k: vertical-line tokens per KV head                  */
   int32_t vl_rows;       /* k rounded up to a multiple of 64                     */
-  int32_t ring_rows;     /* roundup(W, 64) + HYQ_DECODE_WS                       */
+  int32_t ring_rows;     /* roundup(W, 64) + staging                             */
   int32_t n_frozen;      /* quantized tokens written by Freeze (nQ of the prefill)*/
   int32_t cap_blocks;    /* quantized blocks the buffers hold (Freeze + merges)  */
   /* state, set by hyq_freeze and advanced by hyq_decode_append */
   int32_t n_merged;      /* merged blocks, stored after the ceil(nQ/64) frozen ones */
   int32_t ring_head;     /* ring slot of the oldest window token                 */
-  int32_t n_staged;      /* tokens in the staging buffer, 0..HYQ_DECODE_WS       */
-  int32_t reserved;
+  int32_t n_staged;      /* tokens in the staging buffer, 0..staging             */
+  int32_t staging;       /* W_s: staging capacity, a multiple of 64, <= window   */
   int64_t t;             /* tokens cached: N + appended tokens                   */
   /* caller-owned device buffers (byte sizes from hyq_dcache_init) */
   void* k_codes;         /* [B][Hkv][cap_blocks*64][row] row-major, as hyq_quantize */
@@ -277,7 +281,8 @@ typedef struct hyq_dcache_sizes {
  * the prefill calls; bits_kv must be 8 or 4) that will hold up to
  * max_tokens tokens (>= N), zeroes its state and buffer pointers, and
  * returns the byte size of every buffer.
- * Errors: HYQ_EINVAL if W < HYQ_DECODE_WS, N < W or max_tokens < N.
+ * Errors: HYQ_EINVAL if W < W_s, N < W or max_tokens < N, or if
+ * prefill->staging is neither 0 nor a multiple of 64.
  */
 HYQ_API int hyq_dcache_init(const hyq_shape* prefill, int64_t max_tokens, hyq_dcache* cache,
                             hyq_dcache_sizes* sizes);
@@ -295,8 +300,8 @@ HYQ_API int hyq_freeze(const hyq_shape* prefill, const void* Q, const void* K, c
 /*
  * One decode step's key and value rows, k_new and v_new bf16 [B][Hkv][D],
  * enter the staging buffer; when the staging buffer is full they are
- * preceded by the merge of the HYQ_DECODE_WS oldest window tokens into
- * quantized block ceil(n_frozen/64) + n_merged.  Advances the state in
+ * preceded by the merge of the W_s oldest window tokens into quantized
+ * blocks ceil(n_frozen/64) + n_merged, ... (W_s/64 of them).  Advances the state in
  * `cache` (host memory).
  * Errors: HYQ_EINVAL when a merge is due and all cap_blocks blocks are in
  * use (nothing is enqueued and the state is unchanged).

@@ -40,7 +40,7 @@ class HyqError(RuntimeError):
 class _Shape(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("B", "Hq", "Hkv", "L", "D", "window", "budget_ppm", "bits_kv", "block",
-                 "kv_format", "window_mode", "selector")]
+                 "kv_format", "window_mode", "selector", "staging")]
 
 
 class _Sizes(ctypes.Structure):
@@ -52,7 +52,7 @@ class _Sizes(ctypes.Structure):
 
 _DCACHE_INTS = ("B", "Hq", "Hkv", "D", "window", "bits_kv", "kv_format", "n_vl", "vl_rows",
                 "ring_rows", "n_frozen", "cap_blocks", "n_merged", "ring_head", "n_staged",
-                "reserved")
+                "staging")
 _DCACHE_PTRS = ("k_codes", "v_codes", "k_scale", "v_scale", "q_pos", "fp_k", "fp_v", "vl_pos")
 
 
@@ -84,6 +84,7 @@ class Shape:
     kv_format: int = 0      # FMT_INT, FMT_FP8 (bits 8) or FMT_FP4 (bits 4)
     window_mode: int = 0    # WIN_FIXED or WIN_BAND
     selector: int = 0       # SEL_PROXY (Algorithm 1) or SEL_COLMASS (eq. vl_score)
+    staging: int = 0        # decode staging capacity W_s: 0 = DECODE_WS, else a multiple of 64
 
     def c(self) -> _Shape:
         return _Shape(*[int(getattr(self, f.name)) for f in dataclasses.fields(self)])
@@ -369,7 +370,7 @@ class DecodeCache:
         return {n: getattr(self.c, n) for n in ("n_merged", "ring_head", "n_staged", "t")}
 
     def geometry(self) -> dict:
-        return {n: getattr(self.c, n) for n in _DCACHE_INTS if n != "reserved"}
+        return {n: getattr(self.c, n) for n in _DCACHE_INTS}
 
 
 def _decode_rows_ok(cache: DecodeCache, t, name, heads):

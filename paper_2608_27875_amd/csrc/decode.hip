@@ -102,9 +102,11 @@ freeze_gather_kernel(const uint16_t* __restrict__ K, const uint16_t* __restrict_
 }
 
 // ---------------------------------------------------------------------------
-// Append one token (and, first, merge the 64 oldest window tokens into a new
-// quantized block when the staging buffer is full).  blockIdx.y = 0: K,
-// 1: V; one workgroup per (b, j).
+// Append one token (and, first, merge the W_s oldest window tokens into W_s/64
+// new quantized blocks when the staging buffer is full).  blockIdx.y = 0: K,
+// 1: V; blockIdx.z: the merged block; one workgroup per (b, j, K/V, block).
+// Only block 0 writes the new token: with W a multiple of 64 it takes the
+// first slot that block has just quantized.
 // ---------------------------------------------------------------------------
 struct AppendArgs {
   const uint16_t* k_new;
@@ -117,9 +119,9 @@ struct AppendArgs {
   float* vs;
   int32_t* q_pos;
   int nfp, vl_rows, ring_rows, W;
-  int merge;          // 1: quantize ring slots [head, head + 64) into block `blk`
+  int merge;          // 1: quantize ring slots [head + 64z, +64) into block blk + z
   int head;           // ring head before the merge
-  int blk;            // block index of the merged block
+  int blk;            // block index of the first merged block
   int cap_blocks;
   int pos0;           // original position of the oldest window token
   int slot;           // ring slot the new token goes to
@@ -134,17 +136,19 @@ append_kernel(AppendArgs a) {
   __shared__ float red[kQuantThreads / 64];
   const int bj = blockIdx.x;
   const bool is_v = blockIdx.y == 1;
+  const int z = blockIdx.z;
+  const int head = a.head + z * kBlock, blk = a.blk + z;
   if (a.merge) {
     float x[32];
     if (!is_v) {
       const int row = threadIdx.x >> 2, c0 = (threadIdx.x & 3) * 32;
-      const int slot = (a.head + row) % a.ring_rows;
+      const int slot = (head + row) % a.ring_rows;
       load32(a.fk + ((size_t)bj * a.nfp + a.vl_rows + slot) * kHeadDim + c0, x);
       float m = 0.0f;
 #pragma unroll
       for (int e = 0; e < 32; ++e) m = fmaxf(m, fabsf(x[e]));
       const float s = block_max(m, red) / C;
-      uint8_t* dst = a.kc + ((size_t)bj * a.cap_blocks * kBlock + (size_t)a.blk * kBlock + row) * kRow;
+      uint8_t* dst = a.kc + ((size_t)bj * a.cap_blocks * kBlock + (size_t)blk * kBlock + row) * kRow;
       if (BITS == 8) {
         v4u w[2];
 #pragma unroll
@@ -170,20 +174,20 @@ append_kernel(AppendArgs a) {
         }
         *reinterpret_cast<v4u*>(dst + c0 / 2) = w;
       }
-      if (threadIdx.x == 0) a.ks[(size_t)bj * a.cap_blocks + a.blk] = s;
+      if (threadIdx.x == 0) a.ks[(size_t)bj * a.cap_blocks + blk] = s;
       if ((threadIdx.x & 3) == 0)
-        a.q_pos[(size_t)bj * a.cap_blocks * kBlock + (size_t)a.blk * kBlock + row] = a.pos0 + row;
+        a.q_pos[(size_t)bj * a.cap_blocks * kBlock + (size_t)blk * kBlock + row] = a.pos0 + z * kBlock + row;
     } else {
       // V rows are stored channel-major: thread -> (channel d, 32 tokens)
       const int d = threadIdx.x >> 1, r0 = (threadIdx.x & 1) * 32;
       const uint16_t* src = a.fv + ((size_t)bj * kHeadDim + d) * a.nfp + a.vl_rows;
 #pragma unroll
-      for (int e = 0; e < 32; ++e) x[e] = bf16_bits_to_f32(src[(a.head + r0 + e) % a.ring_rows]);
+      for (int e = 0; e < 32; ++e) x[e] = bf16_bits_to_f32(src[(head + r0 + e) % a.ring_rows]);
       float m = 0.0f;
 #pragma unroll
       for (int e = 0; e < 32; ++e) m = fmaxf(m, fabsf(x[e]));
       const float s = block_max(m, red) / C;
-      uint8_t* dst = a.vc + (((size_t)bj * a.cap_blocks + a.blk) * kHeadDim + d) * vRow;
+      uint8_t* dst = a.vc + (((size_t)bj * a.cap_blocks + blk) * kHeadDim + d) * vRow;
       if (BITS == 8) {
         v4u w[2];
 #pragma unroll
@@ -209,10 +213,11 @@ append_kernel(AppendArgs a) {
         }
         *reinterpret_cast<v4u*>(dst + r0 / 2) = w;
       }
-      if (threadIdx.x == 0) a.vs[(size_t)bj * a.cap_blocks + a.blk] = s;
+      if (threadIdx.x == 0) a.vs[(size_t)bj * a.cap_blocks + blk] = s;
     }
     __syncthreads();   // the new token may take a slot the merge has just read
   }
+  if (z != 0) return;
   if (!is_v) {
     if (threadIdx.x < 16) {
       const v4u* s = reinterpret_cast<const v4u*>(a.k_new + (size_t)bj * kHeadDim);
@@ -834,7 +839,7 @@ hipError_t launch_decode_append(const hyq_dcache& c, const uint16_t* k_new, cons
   a.cap_blocks = c.cap_blocks;
   a.pos0 = (int)(c.t - c.n_staged - c.window);
   a.slot = slot;
-  dim3 grid(c.B * c.Hkv, 2);
+  dim3 grid(c.B * c.Hkv, 2, merge ? c.staging / kBlock : 1);
   if (c.kv_format == HYQ_FMT_FP4) append_kernel<4, HYQ_FMT_FP4><<<grid, kQuantThreads, 0, st>>>(a);
   else if (c.kv_format == HYQ_FMT_FP8) append_kernel<8, HYQ_FMT_FP8><<<grid, kQuantThreads, 0, st>>>(a);
   else if (c.bits_kv == 8) append_kernel<8, HYQ_FMT_INT><<<grid, kQuantThreads, 0, st>>>(a);

@@ -53,6 +53,8 @@ int check_shape(const hyq_shape* s, hyq_sizes* z) {
   if (s->selector != HYQ_SEL_PROXY && s->selector != HYQ_SEL_COLMASS)
     return fail(HYQ_EINVAL, "selector must be HYQ_SEL_PROXY or HYQ_SEL_COLMASS (got %d)",
                 s->selector);
+  if (s->staging != 0 && (s->staging < 64 || s->staging % 64))
+    return fail(HYQ_EINVAL, "staging must be 0 or a positive multiple of 64 (got %d)", s->staging);
   if (s->window_mode != HYQ_WIN_FIXED && s->window_mode != HYQ_WIN_BAND)
     return fail(HYQ_EINVAL, "window_mode must be HYQ_WIN_FIXED or HYQ_WIN_BAND (got %d)",
                 s->window_mode);
@@ -116,9 +118,10 @@ int dcache_geometry(const hyq_shape* s, int64_t max_tokens, hyq_dcache* c, hyq_d
   if (rc) return rc;
   if (s->bits_kv == 16)
     return fail(HYQ_EINVAL, "the decode cache needs a quantized format (bits_kv 8 or 4)");
-  if (s->window < HYQ_DECODE_WS)
-    return fail(HYQ_EINVAL, "decode needs window >= %d (the staging buffer merges %d window "
-                "tokens at a time), got %d", HYQ_DECODE_WS, HYQ_DECODE_WS, s->window);
+  const int32_t ws = s->staging ? s->staging : HYQ_DECODE_WS;
+  if (s->window < ws)
+    return fail(HYQ_EINVAL, "decode needs window >= the staging capacity %d (a merge moves that "
+                "many window tokens), got %d", ws, s->window);
   if (s->L < s->window)
     return fail(HYQ_EINVAL, "decode needs a prefill of at least window tokens (L = %d < W = %d)",
                 s->L, s->window);
@@ -135,7 +138,8 @@ int dcache_geometry(const hyq_shape* s, int64_t max_tokens, hyq_dcache* c, hyq_d
   c->kv_format = s->kv_format;
   c->n_vl = z.k;
   c->vl_rows = (int32_t)round_up64(z.k);
-  c->ring_rows = (int32_t)(round_up64(s->window) + HYQ_DECODE_WS);
+  c->ring_rows = (int32_t)(round_up64(s->window) + ws);
+  c->staging = ws;
   c->n_frozen = z.nQ;
   const int64_t nbf = (z.nQ + 63) / 64;
   const int64_t merges = (max_tokens - s->L + HYQ_DECODE_WS - 1) / HYQ_DECODE_WS;
@@ -172,12 +176,13 @@ int check_dcache(const hyq_dcache* c) {
       (c->kv_format == HYQ_FMT_FP4 && c->bits_kv != 4))
     return fail(HYQ_EINVAL, "cache format is invalid (bits_kv %d, kv_format %d)", c->bits_kv,
                 c->kv_format);
-  if (c->window < HYQ_DECODE_WS || c->n_vl < 0 || c->vl_rows != round_up64(c->n_vl) ||
-      c->ring_rows != round_up64(c->window) + HYQ_DECODE_WS || c->n_frozen < 0)
-    return fail(HYQ_EINVAL, "cache geometry is invalid (window, n_vl, vl_rows, ring_rows)");
+  if (c->staging < 64 || c->staging % 64 || c->window < c->staging || c->n_vl < 0 ||
+      c->vl_rows != round_up64(c->n_vl) || c->ring_rows != round_up64(c->window) + c->staging ||
+      c->n_frozen < 0)
+    return fail(HYQ_EINVAL, "cache geometry is invalid (window, staging, n_vl, vl_rows, ring_rows)");
   const int64_t nbf = (c->n_frozen + 63) / 64;
   if (c->n_merged < 0 || nbf + c->n_merged > c->cap_blocks || c->n_staged < 0 ||
-      c->n_staged > HYQ_DECODE_WS || c->ring_head < 0 || c->ring_head >= c->ring_rows ||
+      c->n_staged > c->staging || c->ring_head < 0 || c->ring_head >= c->ring_rows ||
       c->ring_head % 64 != 0 || c->t < (int64_t)c->window)
     return fail(HYQ_EINVAL, "cache state is invalid (n_merged %d, n_staged %d, ring_head %d)",
                 c->n_merged, c->n_staged, c->ring_head);
@@ -318,6 +323,7 @@ HYQ_API int hyq_freeze(const hyq_shape* prefill, const void* Q, const void* K, c
   if (ref.B != cache->B || ref.Hq != cache->Hq || ref.Hkv != cache->Hkv ||
       ref.window != cache->window || ref.bits_kv != cache->bits_kv ||
       ref.kv_format != cache->kv_format || ref.n_vl != cache->n_vl ||
+      ref.staging != cache->staging ||
       ref.n_frozen != cache->n_frozen || cache->cap_blocks < (ref.n_frozen + 63) / 64)
     return fail(HYQ_EINVAL, "cache geometry does not match the prefill shape");
   if (rz.freeze_ws_bytes > 0 && (!ws || ws_bytes < rz.freeze_ws_bytes))
@@ -361,20 +367,20 @@ HYQ_API int hyq_decode_append(hyq_dcache* cache, const void* k_new, const void* 
   const int rc = check_dcache(cache);
   if (rc) return rc;
   if (!k_new || !v_new) return fail(HYQ_EINVAL, "k_new and v_new must be non-NULL");
-  const bool merge = cache->n_staged == HYQ_DECODE_WS;
-  const int nbf = (cache->n_frozen + 63) / 64;
-  if (merge && nbf + cache->n_merged >= cache->cap_blocks)
+  const bool merge = cache->n_staged == cache->staging;
+  const int nbf = (cache->n_frozen + 63) / 64, nb_merge = cache->staging / 64;
+  if (merge && nbf + cache->n_merged + nb_merge > cache->cap_blocks)
     return fail(HYQ_EINVAL, "decode cache full: all %d quantized blocks are in use",
                 cache->cap_blocks);
   if (cache->t >= (int64_t)0x7fffffff) return fail(HYQ_EINVAL, "decode cache full (positions)");
-  const int head = merge ? (cache->ring_head + HYQ_DECODE_WS) % cache->ring_rows : cache->ring_head;
+  const int head = merge ? (cache->ring_head + cache->staging) % cache->ring_rows : cache->ring_head;
   const int staged = merge ? 0 : cache->n_staged;
   const int slot = (head + cache->window + staged) % cache->ring_rows;
   const hipError_t e = hyq::launch_decode_append(*cache, static_cast<const uint16_t*>(k_new),
                                                  static_cast<const uint16_t*>(v_new), merge, slot,
                                                  static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_status(e, "hyq_decode_append launch");
-  if (merge) cache->n_merged += 1;
+  if (merge) cache->n_merged += nb_merge;
   cache->ring_head = head;
   cache->n_staged = staged + 1;
   cache->t += 1;

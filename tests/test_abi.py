@@ -167,17 +167,19 @@ def test_dcache_struct_layout_matches_header(tmp_path):
     assert vals[2 + len(fields):] == [getattr(hyq._DCacheSizes, f).offset for f in hyq._DSIZES]
 
 
-@pytest.mark.parametrize("L,W,ppm,bits,extra", [
-    (32768, 128, 50000, 4, 1024), (1000, 64, 20000, 8, 0), (517, 100, 20000, 4, 200),
-    (200, 64, 1000000, 4, 64), (64, 64, 50000, 8, 140), (450, 96, 0, 8, 1),
+@pytest.mark.parametrize("L,W,ppm,bits,extra,ws", [
+    (32768, 128, 50000, 4, 1024, 0), (1000, 64, 20000, 8, 0, 0), (517, 100, 20000, 4, 200, 0),
+    (200, 64, 1000000, 4, 64, 0), (64, 64, 50000, 8, 140, 0), (450, 96, 0, 8, 1, 0),
+    (32768, 128, 50000, 4, 1024, 128), (700, 200, 30000, 8, 300, 192),
 ])
-def test_dcache_geometry(lib, L, W, ppm, bits, extra):
-    s = _dshape(L=L, window=W, budget_ppm=ppm, bits_kv=bits)
+def test_dcache_geometry(lib, L, W, ppm, bits, extra, ws):
+    s = _dshape(L=L, window=W, budget_ppm=ppm, bits_kv=bits, staging=ws)
     c, z = hyq.hyq_dcache_init(s, L + extra)
     o = orc.sizes(L, W, ppm)
     rup = lambda x: -(-x // 64) * 64
-    assert c.n_vl == o["k"] and c.n_frozen == o["nQ"]
-    assert c.vl_rows == rup(o["k"]) and c.ring_rows == rup(W) + hyq.DECODE_WS
+    Ws = ws or hyq.DECODE_WS
+    assert c.n_vl == o["k"] and c.n_frozen == o["nQ"] and c.staging == Ws
+    assert c.vl_rows == rup(o["k"]) and c.ring_rows == rup(W) + Ws
     assert c.cap_blocks == o["n_kvblk"] + -(-extra // 64)
     assert (c.n_merged, c.ring_head, c.n_staged, c.t) == (0, 0, 0, L)
     BH, nfp, cap = 8, c.vl_rows + c.ring_rows, c.cap_blocks
@@ -191,7 +193,8 @@ def test_dcache_geometry(lib, L, W, ppm, bits, extra):
 
 @pytest.mark.parametrize("kw,max_extra", [
     (dict(window=32), 0), (dict(L=100, window=128), 0), (dict(bits_kv=16), 0),
-    (dict(), -1), (dict(D=64), 0),
+    (dict(), -1), (dict(D=64), 0), (dict(staging=32), 0), (dict(staging=100), 0),
+    (dict(window=128, staging=192), 0), (dict(staging=-64), 0),
 ])
 def test_dcache_bad_geometry_rejected(lib, kw, max_extra):
     s = _dshape(**kw)

@@ -111,7 +111,7 @@ def freeze_both(shape: hyq.Shape, d: dict, max_tokens: int):
     Q, K, V = (gc.to_dev(d[n]) for n in ("Q", "K", "V"))
     hyq.hyq_freeze(shape, Q, K, V, cache)
     oc = orc.freeze(d["Q"], d["K"], d["V"], shape.Hkv, shape.window, shape.budget_ppm,
-                    shape.bits_kv, fmt=_fmt(shape))
+                    shape.bits_kv, fmt=_fmt(shape), staging=shape.staging or hyq.DECODE_WS)
     oc["vl_pos"] = np.asarray(oc["vl_pos"])
     return cache, oc
 
@@ -202,6 +202,38 @@ def test_decode_cache_full_is_an_error():
     torch.cuda.synchronize()
     check_cache(cache, oc)
     check_attention(cache, oc, rng, label="full")
+
+
+# (name, B, Hq, Hkv, N, W, budget_ppm, bits, fmt, staging)
+STAGING = [
+    ("int4_ws128", 1, 8, 2, 700, 128, 30000, 4, hyq.FMT_INT, 128),
+    ("fp8_ws128_w200", 2, 10, 2, 517, 200, 20000, 8, hyq.FMT_FP8, 128),
+    ("fp4_ws192_w200", 1, 16, 2, 1100, 200, 50000, 4, hyq.FMT_FP4, 192),
+]
+
+
+@pytest.mark.parametrize("case", STAGING, ids=[c[0] for c in STAGING])
+def test_decode_staging_capacity(case):
+    """A staging buffer of W_s = 128 or 192 tokens: a full one merges W_s/64
+    blocks at once (oldest first); 2 * W_s + 5 appended tokens, the cache and
+    the attention output checked around each merge."""
+    name, B, Hq, Hkv, N, W, ppm, bits, fmt, ws = case
+    print(f"case {name}", flush=True)
+    shape = hyq.Shape(B=B, Hq=Hq, Hkv=Hkv, L=N, window=W, budget_ppm=ppm, bits_kv=bits,
+                      kv_format=fmt, staging=ws)
+    d = _inputs(name, B, Hq, Hkv, N, W)
+    cache, oc = freeze_both(shape, d, N + 3 * ws)
+    assert cache.c.staging == ws
+    check_cache(cache, oc)
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    for step in range(1, 2 * ws + 6):
+        append_both(cache, oc, rng)
+        if step in (1, ws, ws + 1, ws + 2, 2 * ws + 1, 2 * ws + 5):
+            check_attention(cache, oc, rng, label=name)
+            if step in (ws + 1, 2 * ws + 1):
+                check_cache(cache, oc)
+    assert cache.c.n_merged == 2 * (ws // 64) and cache.c.n_staged == 5
+    check_cache(cache, oc)
 
 
 @pytest.mark.timeout(600)

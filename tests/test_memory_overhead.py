@@ -6,8 +6,8 @@ Strict K4V4 keeps D/2 bytes of K and D/2 of V per token; a token kept in
 bf16 costs 4D bytes, 3D more.  The table's components follow from that, and
 the cache that hyq_dcache_init sizes (host arithmetic only) reproduces them
 once its own choices are accounted for: vertical-line and ring rows padded to
-whole 64-row tiles, a staging buffer of 64 tokens (one quantization block)
-instead of 128, and one float32 scale per 64-token block of K and of V."""
+whole 64-row tiles, the staging capacity (64 tokens by default, 128 as in the
+table), and one float32 scale per 64-token block of K and of V."""
 import os
 
 import pytest
@@ -41,13 +41,15 @@ def test_components_follow_the_bf16_vs_k4v4_cost(N):
 
 
 @pytest.mark.parametrize("N", [8192, 32768])
-def test_cache_sizes_reproduce_the_table(N):
+@pytest.mark.parametrize("Ws", [hyq.DECODE_WS, 128])
+def test_cache_sizes_reproduce_the_table(N, Ws):
     """Overhead of the cache hyq_dcache_init sizes for a Freeze of N tokens
     (no appended token yet), split into the table's components plus this
-    layout's padding and scales."""
+    layout's padding and scales; with the table's 128-token staging buffer
+    and with the default 64."""
     t = _table()
     W, ppm = 128, 50000
-    shape = hyq.Shape(B=1, Hq=32, Hkv=8, L=N, window=W, budget_ppm=ppm, bits_kv=4)
+    shape = hyq.Shape(B=1, Hq=32, Hkv=8, L=N, window=W, budget_ppm=ppm, bits_kv=4, staging=Ws)
     c, z = hyq.hyq_dcache_init(shape, N)
     Hkv = 8
     strict = Hkv * N * D                       # K4V4 bytes of N tokens
@@ -61,9 +63,9 @@ def test_cache_sizes_reproduce_the_table(N):
     # the table's components, from this cache's own token counts
     vl = Hkv * k * 3 * D
     win = Hkv * W * 3 * D
-    staged = Hkv * hyq.DECODE_WS * 4 * D       # empty staging rows (tokens yet to come)
+    staged = Hkv * Ws * 4 * D                  # empty staging rows (tokens yet to come)
     pad_vl = Hkv * (c.vl_rows - k) * 4 * D
-    pad_ring = Hkv * (c.ring_rows - W - hyq.DECODE_WS) * 4 * D
+    pad_ring = Hkv * (c.ring_rows - W - Ws) * 4 * D
     pad_blk = Hkv * (c.cap_blocks * 64 - nq) * D
     assert nq + k + W == N
     total = codes + scales + fp
@@ -72,8 +74,8 @@ def test_cache_sizes_reproduce_the_table(N):
     # vertical lines: k = ceil(5% of the N - W prefix tokens), so slightly under 15%
     assert pct(vl) == pytest.approx(t["vl_tokens"][N], abs=0.3)
     assert pct(win) == pytest.approx(t["local_window"][N], abs=0.05)
-    # a 64-token staging buffer costs half of the table's 128-token one (plus
-    # the bf16 bytes of the tokens not yet appended: 4D instead of 3D)
-    assert pct(staged) == pytest.approx(t["staging_buffer"][N] / 2 * 4 / 3, abs=0.05)
+    # the table prices staged tokens at 3D (bf16 instead of K4V4); rows for
+    # tokens not yet appended cost their whole 4D
+    assert pct(staged) == pytest.approx(t["staging_buffer"][N] * Ws / 128 * 4 / 3, abs=0.05)
     # this layout's own additions stay small
     assert pct(pad_vl + pad_ring + pad_blk + scales) < 2.5
