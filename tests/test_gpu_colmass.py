@@ -124,3 +124,29 @@ def test_colmass_freeze():
     oc["vl_pos"] = np.asarray(oc["vl_pos"])
     td.check_cache(cache, oc)
     td.check_attention(cache, oc, np.random.default_rng(3), label="colmass freeze")
+
+
+@pytest.mark.timeout(600)
+def test_colmass_config5_batch4():
+    """The batch-4, 40q/8kv, 16k workload (2% budget) selected by column
+    mass: every batch and KV head's scores and positions in full, attention
+    on 2 heads x 256 rows of the last batch entry."""
+    shape = dataclasses.replace(gc.shape_of(dict(gen.CONFIGS[5], budget_ppm=20000, bits=8)),
+                                selector=COL)
+    print("config 5 colmass: generating", flush=True)
+    d = gen.generate_config(5, seed=0)
+    g = gc.run_gpu(shape, d, keep_out_on_gpu=True)
+    print("  oracle column mass", flush=True)
+    idx = check_colmass(shape, d, g)
+    qz = orc.quantize(d["Q"], d["K"], d["V"], idx, shape.window, 8)
+    rng = np.random.default_rng(55)
+    heads = [(shape.B - 1, h) for h in sorted(rng.choice(shape.Hq, size=2, replace=False))]
+    rows = gc.sample_rows(shape.L, shape.window, 256, 55)
+    O = orc.attention(d["Q"], d["K"], d["V"], shape.window, 8, idx, qz, heads=heads, rows=rows)
+    import torch
+    out = g["out_dev"]
+    rt = torch.from_numpy(rows).to(out.device)
+    Og = np.stack([out[b, h].index_select(0, rt).cpu().numpy() for b, h in heads])
+    mx, mean = gc.attention_error(Og, O)
+    print(f"  max-abs {mx:.3e} mean-abs {mean:.3e}", flush=True)
+    assert mx <= gc.TOL_MAX and mean <= gc.TOL_MEAN

@@ -128,3 +128,29 @@ def test_fp4_config3_32k():
     mx, mean = gc.attention_error(Og, O)
     print(f"  max-abs {mx:.3e} mean-abs {mean:.3e}", flush=True)
     assert mx <= gc.TOL_MAX and mean <= gc.TOL_MEAN
+
+
+@pytest.mark.timeout(600)
+def test_fp4_config4_128k():
+    """The 131k-token workload (window 512, 0.5% budget) with FP4 codes:
+    selection and every code in full, attention on 2 heads x 256 rows."""
+    cfg = dict(gen.CONFIGS[4], bits=4, fmt=FP4)
+    print("config 4 fp4: generating", flush=True)
+    d = gen.generate_config(4, seed=0)
+    shape = gc.shape_of(cfg)
+    print("  running HIP path", flush=True)
+    g = gc.run_gpu(shape, d, keep_out_on_gpu=True)
+    print("  oracle selection + quantization", flush=True)
+    idx, qz = gc.check_select_quant(shape, d, g)
+    rng = np.random.default_rng(44)
+    heads = [(0, h) for h in sorted(rng.choice(shape.Hq, size=2, replace=False).tolist())]
+    rows = gc.sample_rows(shape.L, shape.window, 256, 44)
+    print(f"  oracle attention on {len(heads)} heads x {len(rows)} rows", flush=True)
+    O = orc.attention(d["Q"], d["K"], d["V"], shape.window, 4, idx, qz, heads=heads, rows=rows)
+    out = g["out_dev"]
+    import torch
+    rt = torch.from_numpy(rows).to(out.device)
+    Og = np.stack([out[b, h].index_select(0, rt).cpu().numpy() for b, h in heads])
+    mx, mean = gc.attention_error(Og, O)
+    print(f"  max-abs {mx:.3e} mean-abs {mean:.3e}", flush=True)
+    assert mx <= gc.TOL_MAX and mean <= gc.TOL_MEAN
