@@ -398,6 +398,32 @@ def main():
     att = [e[2].elapsed_time(e[3]) for e in evs]
     attn_ms = float(np.mean(att))
 
+    def median_ms(run, reps, pre=None, warm=1):
+        """Median over `reps` launches of run(), timed with HIP events on the
+        library's stream; pre() (untimed, e.g. the quantization feeding an
+        attention launch) runs before each."""
+        for _ in range(warm):
+            if pre:
+                pre()
+            run()
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(reps)]
+        for e in ev:
+            if pre:
+                pre()
+            e[0].record(stream)
+            run()
+            e[1].record(stream)
+        torch.cuda.synchronize()
+        return float(np.median([e0.elapsed_time(e1) for e0, e1 in ev]))
+
+    def attn_call(sx, bx):
+        return lambda: hyq.hyq_attn_prefill(sx, Q, K, V, bx["idx"], bx["q_codes"], bx["q_scale"],
+                                            bx["k_codes"], bx["k_scale"], bx["v_codes"],
+                                            bx["v_scale"], bx["kq_pos"], scale, bx["out"],
+                                            out_dtype, stream)
+
     # the same inputs through our own kernel with every key in full precision
     # (bits 16): the in-house exact-attention comparison
     bits16 = None
@@ -407,20 +433,7 @@ def main():
         b16 = hyq.alloc_buffers(s16, dev, out_dtype)
         print("[bench] bits-16 attention", file=sys.stderr, flush=True)
 
-        def step16():
-            hyq.hyq_attn_prefill(s16, Q, K, V, b16["idx"], b16["q_codes"], b16["q_scale"],
-                                 b16["k_codes"], b16["k_scale"], b16["v_codes"], b16["v_scale"],
-                                 b16["kq_pos"], scale, b16["out"], out_dtype, stream)
-        step16()
-        torch.cuda.synchronize()
-        e16 = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(5)]
-        for e in e16:
-            e[0].record(stream)
-            step16()
-            e[1].record(stream)
-        torch.cuda.synchronize()
-        ms16 = float(np.median([e[0].elapsed_time(e[1]) for e in e16]))
+        ms16 = median_ms(attn_call(s16, b16), 5)
         bits16 = {"attention_ms_median": round(ms16, 4),
                   "tflops": round(causal_flops(shape.B, shape.Hq, shape.L, shape.D) /
                                   (ms16 * 1e-3) / 1e12, 2),
@@ -428,32 +441,18 @@ def main():
         del b16
 
     def quant_attn_ms(sx, reps=10):
-        """Median of quantize + attention (timed around the attention only)
-        for another bit-width / format on the same inputs and selection."""
+        """Median attention time for another bit-width / format on the same
+        inputs and selection (each launch after its own quantization)."""
         bx = hyq.alloc_buffers(sx, dev, out_dtype)
         hyq.hyq_select_vertical(sx, Q, K, bx["idx"], None, bx["ws"], stream)
 
-        def stepx(e=None):
+        def quant():
             hyq.hyq_quantize(sx, Q, K, V, bx["idx"], bx["q_codes"], bx["q_scale"],
                              bx["k_codes"], bx["k_scale"], bx["v_codes"], bx["v_scale"],
                              bx["kq_pos"], stream)
-            if e:
-                e[0].record(stream)
-            hyq.hyq_attn_prefill(sx, Q, K, V, bx["idx"], bx["q_codes"], bx["q_scale"],
-                                 bx["k_codes"], bx["k_scale"], bx["v_codes"], bx["v_scale"],
-                                 bx["kq_pos"], scale, bx["out"], out_dtype, stream)
-            if e:
-                e[1].record(stream)
-        for _ in range(2):
-            stepx()
-        torch.cuda.synchronize()
-        ex = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(reps)]
-        for e in ex:
-            stepx(e)
-        torch.cuda.synchronize()
+        ms = median_ms(attn_call(sx, bx), reps, pre=quant, warm=2)
         del bx
-        return float(np.median([e[0].elapsed_time(e[1]) for e in ex]))
+        return ms
 
     # the same inputs with 4-bit K/V codes: int4 (int8 queries, int8 MFMA)
     # and FP4 E2M1 (E4M3 queries, E2M1 keys as the scaled MFMA's 4-bit operand)
@@ -471,35 +470,11 @@ def main():
     # the same inputs with FP8 (E4M3) codes: quantize + attention
     fp8 = None
     if not args.no_fp8 and shape.bits_kv == 8 and fmt == hyq.FMT_INT:
-        s8 = dataclasses.replace(shape, kv_format=hyq.FMT_FP8)
-        b8 = hyq.alloc_buffers(s8, dev, out_dtype)
         print("[bench] fp8 codes", file=sys.stderr, flush=True)
-        hyq.hyq_select_vertical(s8, Q, K, b8["idx"], None, b8["ws"], stream)
-
-        def step8(e=None):
-            hyq.hyq_quantize(s8, Q, K, V, b8["idx"], b8["q_codes"], b8["q_scale"],
-                             b8["k_codes"], b8["k_scale"], b8["v_codes"], b8["v_scale"],
-                             b8["kq_pos"], stream)
-            if e:
-                e[0].record(stream)
-            hyq.hyq_attn_prefill(s8, Q, K, V, b8["idx"], b8["q_codes"], b8["q_scale"],
-                                 b8["k_codes"], b8["k_scale"], b8["v_codes"], b8["v_scale"],
-                                 b8["kq_pos"], scale, b8["out"], out_dtype, stream)
-            if e:
-                e[1].record(stream)
-        for _ in range(2):
-            step8()
-        torch.cuda.synchronize()
-        e8 = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(10)]
-        for e in e8:
-            step8(e)
-        torch.cuda.synchronize()
-        ms8 = float(np.median([e[0].elapsed_time(e[1]) for e in e8]))
+        ms8 = quant_attn_ms(dataclasses.replace(shape, kv_format=hyq.FMT_FP8))
         tf8 = causal_flops(shape.B, shape.Hq, shape.L, shape.D) / (ms8 * 1e-3) / 1e12
         fp8 = {"attention_ms_median": round(ms8, 4), "tflops": round(tf8, 2),
                "frac_fp8_peak": round(tf8 / INT8_PEAK_TOPS, 4)}
-        del b8
 
     # the same inputs and codes with the per-query window of eq. (win_def):
     # attention only (selection and quantization are the same)
@@ -508,21 +483,7 @@ def main():
         sb = dataclasses.replace(shape, window_mode=hyq.WIN_BAND)
         print("[bench] per-query window (band) attention", file=sys.stderr, flush=True)
 
-        def stepb():
-            hyq.hyq_attn_prefill(sb, Q, K, V, bufs["idx"], bufs["q_codes"], bufs["q_scale"],
-                                 bufs["k_codes"], bufs["k_scale"], bufs["v_codes"],
-                                 bufs["v_scale"], bufs["kq_pos"], scale, bufs["out"], out_dtype,
-                                 stream)
-        stepb()
-        torch.cuda.synchronize()
-        eb = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(10)]
-        for e in eb:
-            e[0].record(stream)
-            stepb()
-            e[1].record(stream)
-        torch.cuda.synchronize()
-        msb = float(np.median([e[0].elapsed_time(e[1]) for e in eb]))
+        msb = median_ms(attn_call(sb, bufs), 10)
         tfb = causal_flops(shape.B, shape.Hq, shape.L, shape.D) / (msb * 1e-3) / 1e12
         band = {"attention_ms_median": round(msb, 4), "tflops": round(tfb, 2),
                 "frac_int8_peak": round(tfb / INT8_PEAK_TOPS, 4)}
@@ -535,18 +496,8 @@ def main():
         bc = hyq.alloc_buffers(sc, dev, out_dtype)
         print("[bench] column-mass selector", file=sys.stderr, flush=True)
 
-        def stepc():
-            hyq.hyq_select_vertical(sc, Q, K, bc["idx"], None, bc["ws"], stream)
-        stepc()
-        torch.cuda.synchronize()
-        ec = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(10)]
-        for e in ec:
-            e[0].record(stream)
-            stepc()
-            e[1].record(stream)
-        torch.cuda.synchronize()
-        msc = float(np.median([e[0].elapsed_time(e[1]) for e in ec]))
+        msc = median_ms(lambda: hyq.hyq_select_vertical(sc, Q, K, bc["idx"], None, bc["ws"],
+                                                        stream), 10)
         # two QK^T passes over the tail rows: every causal key, then the prefix
         tr = min(shape.window, shape.L)
         rows = shape.B * shape.Hq * tr
