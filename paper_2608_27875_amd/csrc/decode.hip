@@ -28,6 +28,8 @@
 #include "hyq_internal.h"
 #include "quant_dev.h"
 
+#include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 namespace hyq {
@@ -246,7 +248,7 @@ struct DecodeArgs {
   int nbf;          // frozen blocks; block nbf-1 holds n_last tokens
   int n_last;
   int n_vl, vl_rows, nfp, ring_head, ring_rows, ring_valid;
-  int S_q, S_f, U;  // quantized splits, full-precision splits, blocks per wave
+  int S_q, S_f;     // quantized splits, full-precision splits
   float c_log2;     // softmax_scale * log2(e)
 };
 
@@ -604,8 +606,11 @@ decode_attn_kernel(DecodeArgs a, const float* __restrict__ ks, const float* __re
   st.eref = -1000;
 
   if (split < a.S_q) {
-    const int first = split * kDecWaves * a.U + w;
-    const int n_my = first < a.nbq ? min(a.U, (a.nbq - first + kDecWaves - 1) / kDecWaves) : 0;
+    // an even share of the quantized blocks: wave gw of the nw = S_q * 4
+    // takes the consecutive blocks [gw * nbq / nw, (gw + 1) * nbq / nw)
+    const int nw = a.S_q * kDecWaves, gw = split * kDecWaves + w;
+    const int first = (int)((int64_t)gw * a.nbq / nw);
+    const int n_my = (int)((int64_t)(gw + 1) * a.nbq / nw) - first;
     QRegs<BITS> r0, r1;
     load_q<BITS == 4 ? kMapI4 : kMapB8>(qw, qrow, qok, G);   // first: waits for it never wait for codes
     if (n_my > 0) load_block<BITS>(r0, a, ks, vs, bj, first, hl, G);
@@ -649,7 +654,7 @@ decode_attn_kernel(DecodeArgs a, const float* __restrict__ ks, const float* __re
     // unconditional, which keeps each wait for a block's codes from also
     // waiting for the prefetched block
     auto proc = [&](const QRegs<BITS>& r, int i) {
-      const int blk = first + kDecWaves * i;
+      const int blk = first + i;
       const int n_valid = blk == a.nbf - 1 ? a.n_last : kBlock;
       // keep the scheduler from starting the next block's conversions (and
       // so waiting for its loads) inside this one
@@ -659,26 +664,28 @@ decode_attn_kernel(DecodeArgs a, const float* __restrict__ ks, const float* __re
     };
     int i = 0;
     for (; i + 2 < n_my; i += 2) {
-      load_block<BITS>(r1, a, ks, vs, bj, first + kDecWaves * (i + 1), hl, G);
+      load_block<BITS>(r1, a, ks, vs, bj, first + i + 1, hl, G);
       proc(r0, i);
-      load_block<BITS>(r0, a, ks, vs, bj, first + kDecWaves * (i + 2), hl, G);
+      load_block<BITS>(r0, a, ks, vs, bj, first + i + 2, hl, G);
       proc(r1, i + 1);
     }
     if (i + 1 < n_my) {
-      load_block<BITS>(r1, a, ks, vs, bj, first + kDecWaves * (i + 1), hl, G);
+      load_block<BITS>(r1, a, ks, vs, bj, first + i + 1, hl, G);
       proc(r0, i);
       proc(r1, i + 1);
     } else if (i < n_my) {
       proc(r0, i);
     }
   } else {
-    const int tile = (split - a.S_q) * kDecWaves + w;
-    if (tile < a.nfp / kBlock) {
+    // full-precision tiles tile, tile + 4 S_f, ...
+    const int nft = a.nfp / kBlock;
+    int tile = (split - a.S_q) * kDecWaves + w;
+    if (tile < nft) {
       load_q<kMapBF16>(qw, qrow, qok, G);
       v8bf qb[4];
 #pragma unroll
       for (int s = 0; s < 4; ++s) qb[s] = __builtin_bit_cast(v8bf, qw[s]);
-      process_fp_tile(st, a, bj, tile, qb, hl, G);
+      for (; tile < nft; tile += a.S_f * kDecWaves) process_fp_tile(st, a, bj, tile, qb, hl, G);
     }
   }
 
@@ -788,15 +795,66 @@ decode_combine_kernel(const float* __restrict__ part, void* __restrict__ out, in
 
 // ---- host launchers -------------------------------------------------------
 
+// Compute units of the current device (cached per device).
+static int device_cus() {
+  constexpr int kMaxDev = 64;
+  static std::atomic<int> cus[kMaxDev];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) return 256;
+  int n = cus[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+      n = 256;
+    cus[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
+// Splits of the decode launch.  By default a wave takes about 32 KB of codes
+// (4 int4 or 2 8-bit blocks, as much as one full-precision tile).  The decode
+// loop is bound by each SIMD's vector ALU, so a launch takes about as long as
+// its busiest SIMD: (workgroups on the busiest CU) x (bytes of the busiest
+// wave).  When the default leaves the CUs unevenly loaded (312 workgroups on
+// 256 CUs: some CUs run two), the launch is reshaped to k workgroups per CU
+// with fewer, longer splits, and the full-precision tiles per wave chosen so
+// that no wave reads many more bytes than the others; the shape with the
+// smallest busiest-SIMD bytes wins.  Splits never exceed the default, which
+// bounds the workspace.
 DecodeSplit decode_split(const hyq_dcache& c) {
   DecodeSplit d;
   const int nbf = (c.n_frozen + kBlock - 1) / kBlock;
   d.nbq = nbf + c.n_merged;
-  // about 32 KB of codes per wave, as much as one full-precision tile
-  d.U = c.bits_kv == 4 ? 4 : 2;
-  d.S_q = (d.nbq + kDecWaves * d.U - 1) / (kDecWaves * d.U);
+  const int u = c.bits_kv == 4 ? 4 : 2;
+  d.S_q = (d.nbq + kDecWaves * u - 1) / (kDecWaves * u);
   const int nft = (c.vl_rows + c.ring_rows) / kBlock;
   d.S_f = (nft + kDecWaves - 1) / kDecWaves;
+  if (d.S_q == 0) return d;
+  const int64_t heads = (int64_t)c.B * c.Hkv;
+  const int64_t n_cu = device_cus();
+  const int64_t blk_bytes = 2 * kBlock * kHeadDim * c.bits_kv / 8;   // K and V codes
+  const int64_t tile_bytes = 2 * kBlock * kHeadDim * 2;              // K and V bf16 rows
+  auto wave_bytes = [&](int s_q, int s_f) {
+    const int64_t blks = (d.nbq + kDecWaves * s_q - 1) / ((int64_t)kDecWaves * s_q);
+    const int64_t tiles = s_f ? (nft + kDecWaves * s_f - 1) / ((int64_t)kDecWaves * s_f) : 0;
+    return std::max(blks * blk_bytes, tiles * tile_bytes);
+  };
+  const int64_t rounds = ((d.S_q + d.S_f) * heads + n_cu - 1) / n_cu;
+  int64_t best = rounds * wave_bytes(d.S_q, d.S_f);
+  for (int64_t k = 1; k < rounds && k <= 32; ++k) {
+    const int64_t fit = k * n_cu / heads;   // workgroups per KV head
+    for (int f = 1; f <= 4; ++f) {          // full-precision tiles per wave
+      const int s_f = (nft + kDecWaves * f - 1) / (kDecWaves * f);
+      const int s_q = (int)std::min<int64_t>(d.S_q, fit - s_f);
+      if (s_q < 1 || s_f > d.S_f) continue;
+      const int64_t cost = k * wave_bytes(s_q, s_f);
+      if (cost < best) {
+        best = cost;
+        d.S_q = s_q;
+        d.S_f = s_f;
+      }
+    }
+  }
   return d;
 }
 
@@ -872,7 +930,6 @@ hipError_t launch_decode_attn(const hyq_dcache& c, const uint16_t* q, float soft
   a.ring_valid = c.window + c.n_staged;
   a.S_q = d.S_q;
   a.S_f = d.S_f;
-  a.U = d.U;
   a.c_log2 = softmax_scale * 1.4426950408889634f;
   const int S = d.S_q + d.S_f;
   dim3 grid(S, c.B * c.Hkv);

@@ -49,7 +49,7 @@ void launch_quant_kv(int bits, int fmt, const uint16_t* K, const uint16_t* V,
 // Decode: split of the sequence axis (blocks per wave U, quantized splits
 // S_q, full-precision splits S_f), workspace size, and the launches.
 struct DecodeSplit {
-  int nbq, U, S_q, S_f;
+  int nbq, S_q, S_f;   // quantized blocks; quantized and full-precision workgroups per KV head
 };
 constexpr int kDecodePartFloats = 132;   // one partial: acc[128], m, l, padding
 DecodeSplit decode_split(const hyq_dcache& c);

@@ -237,14 +237,18 @@ def test_decode_staging_capacity(case):
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("fmt,ws", [(hyq.FMT_INT, 128), (hyq.FMT_FP4, 64)],
-                         ids=["int4_ws128", "fp4_ws64"])
-def test_decode_32k_k4v4_top5_w128(fmt, ws):
+@pytest.mark.parametrize("bits,fmt,ws", [(4, hyq.FMT_INT, 128), (4, hyq.FMT_FP4, 64),
+                                         (8, hyq.FMT_INT, 128)],
+                         ids=["int4_ws128", "fp4_ws64", "int8_ws128"])
+def test_decode_32k_k4v4_top5_w128(bits, fmt, ws):
     """The paper's decode-latency workload: batch 1, 32 query / 8 KV heads,
     d 128, 32k-token prefix, K4V4, top-5% vertical lines, window 128 (with
-    the 128-token staging buffer the benchmark uses, and with the default)."""
+    the 128-token staging buffer the benchmark uses, and with the default);
+    also with 8-bit codes.  On a 256-CU device all three launch one
+    workgroup per CU with uneven shares of the quantized blocks, and the
+    8-bit one gives each full-precision wave two tiles."""
     N, W = 32768, 128
-    shape = hyq.Shape(B=1, Hq=32, Hkv=8, L=N, window=W, budget_ppm=50000, bits_kv=4,
+    shape = hyq.Shape(B=1, Hq=32, Hkv=8, L=N, window=W, budget_ppm=50000, bits_kv=bits,
                       kv_format=fmt, staging=ws)
     print("generating", flush=True)
     d = gen.generate(0, 7, B=1, Hq=32, Hkv=8, L=N, D=128, W=W, plant=0.05,
@@ -260,6 +264,25 @@ def test_decode_32k_k4v4_top5_w128(fmt, ws):
     assert cache.c.n_merged == ws // 64
     check_attention(cache, oc, rng, label="32k")
     check_cache(cache, oc)
+
+
+@pytest.mark.timeout(300)
+def test_decode_batch4_reshaped_split():
+    """Batch 4, 32 query / 8 KV heads, 4k prefix, int8: the default split
+    (320 workgroups) is cut to one workgroup per CU on a 256-CU device, each
+    wave taking 2 or 3 consecutive quantized blocks; checked through one merge."""
+    name, B, Hq, Hkv, N, W = "b4_reshaped", 4, 32, 8, 4096, 128
+    print(f"case {name}", flush=True)
+    shape = hyq.Shape(B=B, Hq=Hq, Hkv=Hkv, L=N, window=W, budget_ppm=50000, bits_kv=8)
+    d = _inputs(name, B, Hq, Hkv, N, W)
+    cache, oc = freeze_both(shape, d, N + 128)
+    check_cache(cache, oc)
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    check_attention(cache, oc, rng, label=name)
+    for _ in range(65):
+        append_both(cache, oc, rng)
+    assert cache.c.n_merged == 1
+    check_attention(cache, oc, rng, label=name)
 
 
 def test_decode_attention_in_a_hip_graph():
