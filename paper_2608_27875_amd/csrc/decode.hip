@@ -728,11 +728,12 @@ decode_attn_kernel(DecodeArgs a, const float* __restrict__ ks, const float* __re
   }
 }
 
-// ReduceSoftmax over the S partials of each (b, h): one workgroup per query
-// row.  Thread -> (share ph of the partials, 4 channels): an online max over
-// its share (all loads independent, issued together), then the 16 shares of
-// each channel quad merged through LDS.
-constexpr int kCombThreads = 512;
+// ReduceSoftmax over the S partials of each (b, h): one workgroup of two waves
+// per query row.  Thread -> (share ph of the partials, 4 channels): an online
+// max over its share (loads issued 8 deep), then the 4 shares of each channel
+// quad merged through LDS.  The kernel is bound by latency, not bytes: fewer,
+// longer shares beat more threads.
+constexpr int kCombThreads = 128;
 constexpr int kCombShares = kCombThreads / (kHeadDim / 4);
 __global__ void __launch_bounds__(kCombThreads)
 decode_combine_kernel(const float* __restrict__ part, void* __restrict__ out, int Hq, int Hkv,
@@ -748,7 +749,7 @@ decode_combine_kernel(const float* __restrict__ part, void* __restrict__ out, in
   const size_t stride = (size_t)g * kPartStride;
   float M = kMinusBigD, L = 0.0f;
   v4f acc = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll 4
+#pragma unroll 8
   for (int s = ph; s < S; s += kCombShares) {
     const float* p = base + s * stride;
     const v2u ml = *reinterpret_cast<const v2u*>(p + kHeadDim);
