@@ -578,10 +578,10 @@ __device__ __forceinline__ void process_fp_tile(WaveState& st, const DecodeArgs&
   }
 }
 
-// Grid (S_q + S_f, B*Hkv): workgroups x < S_q take 4U consecutive quantized
-// blocks of KV head (b, j) (wave w: blocks w, w+4, ...), the others 4
-// full-precision tiles (one per wave).  Each workgroup writes one partial
-// (acc[128], m, l) per query head of the group.
+// Grid (S_q + S_f, B*Hkv): in workgroups x < S_q each of the 4 S_q waves of
+// KV head (b, j) takes an even share of consecutive quantized blocks; in the
+// others wave t takes the full-precision tiles t, t + 4 S_f, ...  Each
+// workgroup writes one partial (acc[128], m, l) per query head of the group.
 template <int BITS, int FMT>
 __global__ void __launch_bounds__(kDecThreads, 2)
 decode_attn_kernel(DecodeArgs a, const float* __restrict__ ks, const float* __restrict__ vs) {

@@ -46,8 +46,8 @@ void launch_quant_kv(int bits, int fmt, const uint16_t* K, const uint16_t* V,
                      float* v_scale, int L, int nQ, int n_blocks, int blk_stride, int BHkv,
                      hipStream_t st);
 
-// Decode: split of the sequence axis (blocks per wave U, quantized splits
-// S_q, full-precision splits S_f), workspace size, and the launches.
+// Decode: split of the sequence axis (quantized splits S_q, full-precision
+// splits S_f, per KV head), workspace size, and the launches.
 struct DecodeSplit {
   int nbq, S_q, S_f;   // quantized blocks; quantized and full-precision workgroups per KV head
 };
