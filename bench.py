@@ -259,11 +259,14 @@ def decode_section(layers, steps):
 
 
 def main():
+    from paper_2608_27875_amd import gen   # the named workloads (numpy only)
+
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=3, help="workload id (1-5); 3 = 32k GQA")
+    ap.add_argument("--workload", default=gen.GQA_32K, choices=sorted(gen.WORKLOADS),
+                    help="named synthetic workload (default: the 32k GQA prefill)")
     ap.add_argument("--bits", type=int, default=None, help="override K/V bit-width (16, 8, 4)")
     ap.add_argument("--budget-ppm", type=int, default=None)
     ap.add_argument("--out-bf16", action="store_true")
@@ -272,7 +275,7 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--hq", type=int, default=None,
                     help="keep only the first HQ query heads (with their KV heads): e.g. --hq 4 "
-                         "is one GPU's share of config 3 under 8-way head sharding")
+                         "is one GPU's share of the 32k workload under 8-way head sharding")
     ap.add_argument("--no-bits16", action="store_true",
                     help="skip the full-precision (bits 16) attention of the same inputs")
     ap.add_argument("--fmt", choices=("int", "fp8", "fp4"), default="int",
@@ -303,7 +306,6 @@ def main():
     import torch
 
     import paper_2608_27875_amd as hyq
-    from paper_2608_27875_amd import gen
 
     if args.decode_only:
         if args.traffic_probe:
@@ -312,13 +314,13 @@ def main():
         print(json.dumps({"decode": decode_section(args.decode_layers, args.steps)}), flush=True)
         return
 
-    cfg = dict(gen.CONFIGS[args.config])
+    cfg = gen.workload(args.workload)
     if args.bits is not None:
         cfg["bits"] = args.bits
     if args.budget_ppm is not None:
         cfg["budget_ppm"] = args.budget_ppm
-    print(f"[bench] generating config {args.config}: {cfg}", file=sys.stderr, flush=True)
-    d = gen.generate_config(args.config, seed=args.seed)
+    print(f"[bench] generating workload {args.workload}: {cfg}", file=sys.stderr, flush=True)
+    d = gen.generate_workload(args.workload, seed=args.seed)
     dev = torch.device("cuda:0")
 
     def t(x):

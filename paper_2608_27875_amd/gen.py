@@ -19,18 +19,30 @@ import numpy as np
 
 OUTLIER_CHANNELS = (3, 47, 85, 122)
 
-# The five workloads: shapes, window, vertical budget (parts per million of
-# the non-window prefix), K/V bit-width and the planted vertical-line fraction.
-CONFIGS = {
-    1: dict(B=1, Hq=1, Hkv=1, L=1024, D=128, W=64, budget_ppm=20000, bits=8, plant=0.01),
-    2: dict(B=1, Hq=32, Hkv=8, L=8192, D=128, W=128, budget_ppm=20000, bits=8, plant=0.01),
-    3: dict(B=1, Hq=32, Hkv=8, L=32768, D=128, W=256, budget_ppm=10000, bits=8, plant=0.01),
-    4: dict(B=1, Hq=32, Hkv=8, L=131072, D=128, W=512, budget_ppm=5000, bits=8, plant=0.01),
-    5: dict(B=4, Hq=40, Hkv=8, L=16384, D=128, W=256, budget_ppm=20000, bits=8, plant=0.05),
+# The five workloads, named by shape: batch, heads, length, window, vertical
+# budget (parts per million of the non-window prefix), K/V bit-width, the
+# planted vertical-line fraction, and the generator stream that separates
+# workloads drawn with the same seed.
+WORKLOADS = {
+    "gqa1q1kv_B1_L1024": dict(stream=1, B=1, Hq=1, Hkv=1, L=1024, D=128, W=64,
+                              budget_ppm=20000, bits=8, plant=0.01),
+    "gqa32q8kv_B1_L8192": dict(stream=2, B=1, Hq=32, Hkv=8, L=8192, D=128, W=128,
+                               budget_ppm=20000, bits=8, plant=0.01),
+    "gqa32q8kv_B1_L32768": dict(stream=3, B=1, Hq=32, Hkv=8, L=32768, D=128, W=256,
+                                budget_ppm=10000, bits=8, plant=0.01),
+    "gqa32q8kv_B1_L131072": dict(stream=4, B=1, Hq=32, Hkv=8, L=131072, D=128, W=512,
+                                 budget_ppm=5000, bits=8, plant=0.01),
+    "gqa40q8kv_B4_L16384": dict(stream=5, B=4, Hq=40, Hkv=8, L=16384, D=128, W=256,
+                                budget_ppm=20000, bits=8, plant=0.05),
 }
-# Config 5 is a sweep over these two axes.
-SWEEP5_BUDGETS = (5000, 20000, 50000)
-SWEEP5_BITS = (8, 4)
+SMALL = "gqa1q1kv_B1_L1024"
+GQA_8K = "gqa32q8kv_B1_L8192"
+GQA_32K = "gqa32q8kv_B1_L32768"      # the benchmarked prefill workload
+GQA_128K = "gqa32q8kv_B1_L131072"
+BATCH4_16K = "gqa40q8kv_B4_L16384"
+# The batch-4 16k workload is run as a sweep over these two axes.
+BATCH4_BUDGETS = (5000, 20000, 50000)
+BATCH4_BITS = (8, 4)
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -53,7 +65,7 @@ def generate(seed: int, stream: int, B: int, Hq: int, Hkv: int, L: int, D: int,
     Returns a dict with uint16 (bf16 bit pattern) arrays ``Q`` [B,Hq,L,D],
     ``K`` and ``V`` [B,Hkv,L,D], and ``planted``: a list over (b, j) of the
     sorted planted key positions.  ``stream`` separates workloads that share a
-    seed (configs use their number).
+    seed (each named workload has its own).
     """
     if Hq % Hkv:
         raise ValueError("Hq must be a multiple of Hkv")
@@ -85,12 +97,18 @@ def generate(seed: int, stream: int, B: int, Hq: int, Hkv: int, L: int, D: int,
     return dict(Q=Q, K=K, V=V, planted=planted)
 
 
-def generate_config(cfg_id: int, seed: int = 0, **overrides):
-    """Inputs for one of the five named workloads (``overrides`` may change the
-    budget or bit-width of the sweep config; the drawn tensors do not depend on
-    them)."""
-    cfg = dict(CONFIGS[cfg_id])
+def workload(name: str, **overrides) -> dict:
+    """Parameters of a named workload (without its generator stream)."""
+    cfg = {k: v for k, v in WORKLOADS[name].items() if k != "stream"}
     cfg.update(overrides)
-    data = generate(seed, cfg_id, **cfg)
+    return cfg
+
+
+def generate_workload(name: str, seed: int = 0, **overrides):
+    """Inputs for one of the named workloads (``overrides`` may change the
+    budget or bit-width of the batch-4 sweep; the drawn tensors do not depend
+    on them)."""
+    cfg = workload(name, **overrides)
+    data = generate(seed, WORKLOADS[name]["stream"], **cfg)
     data["cfg"] = cfg
     return data

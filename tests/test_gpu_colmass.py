@@ -86,13 +86,13 @@ def test_colmass_small_full_path(case):
 
 
 @pytest.mark.timeout(300)
-def test_colmass_config3_32k():
+def test_colmass_32k():
     """The 32k GQA workload selected by column mass (the 256 tail queries of
     each of the 32 heads against 32k keys): scores and positions in full,
     attention on 4 heads x 256 rows."""
-    shape = dataclasses.replace(gc.shape_of(gen.CONFIGS[3]), selector=COL)
-    print("config 3 colmass: generating", flush=True)
-    d = gen.generate_config(3, seed=0)
+    shape = dataclasses.replace(gc.shape_of(gen.workload(gen.GQA_32K)), selector=COL)
+    print("32k colmass: generating", flush=True)
+    d = gen.generate_workload(gen.GQA_32K, seed=0)
     g = gc.run_gpu(shape, d, keep_out_on_gpu=True)
     print("  oracle column mass", flush=True)
     idx = check_colmass(shape, d, g)
@@ -127,14 +127,14 @@ def test_colmass_freeze():
 
 
 @pytest.mark.timeout(600)
-def test_colmass_config5_batch4():
+def test_colmass_batch4_16k():
     """The batch-4, 40q/8kv, 16k workload (2% budget) selected by column
     mass: every batch and KV head's scores and positions in full, attention
     on 2 heads x 256 rows of the last batch entry."""
-    shape = dataclasses.replace(gc.shape_of(dict(gen.CONFIGS[5], budget_ppm=20000, bits=8)),
+    shape = dataclasses.replace(gc.shape_of(gen.workload(gen.BATCH4_16K, budget_ppm=20000, bits=8)),
                                 selector=COL)
-    print("config 5 colmass: generating", flush=True)
-    d = gen.generate_config(5, seed=0)
+    print("batch-4 16k colmass: generating", flush=True)
+    d = gen.generate_workload(gen.BATCH4_16K, seed=0)
     g = gc.run_gpu(shape, d, keep_out_on_gpu=True)
     print("  oracle column mass", flush=True)
     idx = check_colmass(shape, d, g)

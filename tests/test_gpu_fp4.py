@@ -105,11 +105,11 @@ def test_fp4_deterministic():
 
 
 @pytest.mark.timeout(300)
-def test_fp4_config3_32k():
+def test_fp4_32k():
     """The 32k GQA workload with FP4 codes (4 heads x 512 sampled rows)."""
-    cfg = dict(gen.CONFIGS[3], bits=4, fmt=FP4)
-    print("config 3 fp4: generating", flush=True)
-    d = gen.generate_config(3, seed=0)
+    cfg = gen.workload(gen.GQA_32K, bits=4, fmt=FP4)
+    print("32k fp4: generating", flush=True)
+    d = gen.generate_workload(gen.GQA_32K, seed=0)
     shape = gc.shape_of(cfg)
     print("  running HIP path", flush=True)
     g = gc.run_gpu(shape, d, keep_out_on_gpu=True)
@@ -131,12 +131,12 @@ def test_fp4_config3_32k():
 
 
 @pytest.mark.timeout(600)
-def test_fp4_config4_128k():
+def test_fp4_128k():
     """The 131k-token workload (window 512, 0.5% budget) with FP4 codes:
     selection and every code in full, attention on 2 heads x 256 rows."""
-    cfg = dict(gen.CONFIGS[4], bits=4, fmt=FP4)
-    print("config 4 fp4: generating", flush=True)
-    d = gen.generate_config(4, seed=0)
+    cfg = gen.workload(gen.GQA_128K, bits=4, fmt=FP4)
+    print("128k fp4: generating", flush=True)
+    d = gen.generate_workload(gen.GQA_128K, seed=0)
     shape = gc.shape_of(cfg)
     print("  running HIP path", flush=True)
     g = gc.run_gpu(shape, d, keep_out_on_gpu=True)

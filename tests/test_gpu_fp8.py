@@ -120,18 +120,18 @@ def _check_big(cfg, d, n_heads, n_rows, seed):
 
 
 @pytest.mark.timeout(300)
-def test_fp8_config3_32k():
+def test_fp8_32k():
     """The 32k GQA workload with FP8 codes (4 heads x 512 sampled rows)."""
-    cfg = dict(gen.CONFIGS[3], fmt=FP8)
-    print("config 3 fp8: generating", flush=True)
-    d = gen.generate_config(3, seed=0)
+    cfg = gen.workload(gen.GQA_32K, fmt=FP8)
+    print("32k fp8: generating", flush=True)
+    d = gen.generate_workload(gen.GQA_32K, seed=0)
     _check_big(cfg, d, 4, 512, seed=33)
 
 
 @pytest.mark.timeout(300)
-def test_fp8_config5_sweep_point():
-    """Config 5 (B = 4, 40q/8kv, 16k) at the 2% budget with FP8 codes."""
-    cfg = dict(gen.CONFIGS[5], budget_ppm=20000, bits=8, fmt=FP8)
-    print("config 5 fp8: generating", flush=True)
-    d = gen.generate_config(5, seed=0)
+def test_fp8_batch4_16k():
+    """The batch-4 workload (40q/8kv, 16k) at the 2% budget with FP8 codes."""
+    cfg = gen.workload(gen.BATCH4_16K, budget_ppm=20000, bits=8, fmt=FP8)
+    print("batch-4 16k fp8: generating", flush=True)
+    d = gen.generate_workload(gen.BATCH4_16K, seed=0)
     _check_big(cfg, d, 2, 256, seed=55)

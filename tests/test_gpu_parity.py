@@ -95,11 +95,10 @@ def test_deterministic_and_bf16_output():
     np.testing.assert_array_equal(gb["out"], ref)
 
 
-def _big(cfg_id, n_heads, n_rows, seed=0, **over):
-    cfg = dict(gen.CONFIGS[cfg_id])
-    cfg.update(over)
-    print(f"config {cfg_id} {over}: generating", flush=True)
-    d = gen.generate_config(cfg_id, seed=seed)
+def _big(name, n_heads, n_rows, seed=0, **over):
+    cfg = gen.workload(name, **over)
+    print(f"{name} {over}: generating", flush=True)
+    d = gen.generate_workload(name, seed=seed)
     return cfg, d
 
 
@@ -127,35 +126,34 @@ def _check_big(cfg, d, n_heads, n_rows, seed):
 
 
 @pytest.mark.timeout(300)
-def test_config2_8k_gqa():
-    cfg, d = _big(2, 32, 256)
+def test_gqa_8k():
+    cfg, d = _big(gen.GQA_8K, 32, 256)
     _check_big(cfg, d, 32, 256, seed=2)
 
 
 @pytest.mark.timeout(300)
-def test_config3_32k_headline():
+def test_gqa_32k_benchmarked():
     """The workload and launch configuration the benchmark times (float32 out)."""
-    cfg, d = _big(3, 4, 512)
+    cfg, d = _big(gen.GQA_32K, 4, 512)
     _check_big(cfg, d, 4, 512, seed=3)
 
 
 @pytest.mark.timeout(600)
-def test_config4_128k():
-    cfg, d = _big(4, 2, 256)
+def test_gqa_128k():
+    cfg, d = _big(gen.GQA_128K, 2, 256)
     _check_big(cfg, d, 2, 256, seed=4)
 
 
 @pytest.fixture(scope="module")
-def cfg5_data():
-    print("config 5: generating", flush=True)
-    return gen.generate_config(5, seed=0)
+def batch4_data():
+    print("batch-4 16k: generating", flush=True)
+    return gen.generate_workload(gen.BATCH4_16K, seed=0)
 
 
 @pytest.mark.timeout(300)
-@pytest.mark.parametrize("ppm", gen.SWEEP5_BUDGETS)
-@pytest.mark.parametrize("bits", gen.SWEEP5_BITS)
-def test_config5_sweep(cfg5_data, ppm, bits):
-    cfg = dict(gen.CONFIGS[5])
-    cfg.update(budget_ppm=ppm, bits=bits)
-    print(f"config 5 budget {ppm} bits {bits}", flush=True)
-    _check_big(cfg, cfg5_data, 2, 256, seed=5 + ppm + bits)
+@pytest.mark.parametrize("ppm", gen.BATCH4_BUDGETS)
+@pytest.mark.parametrize("bits", gen.BATCH4_BITS)
+def test_batch4_16k_sweep(batch4_data, ppm, bits):
+    cfg = gen.workload(gen.BATCH4_16K, budget_ppm=ppm, bits=bits)
+    print(f"batch-4 16k budget {ppm} bits {bits}", flush=True)
+    _check_big(cfg, batch4_data, 2, 256, seed=5 + ppm + bits)

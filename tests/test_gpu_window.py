@@ -57,13 +57,13 @@ def test_band_small_full_parity(case):
 
 
 @pytest.mark.timeout(300)
-def test_band_config3_32k():
+def test_band_32k():
     """The 32k GQA workload with the per-query window (4 heads x 512 rows,
     always including rows W-1, W, P-1, P and L-1)."""
-    cfg = dict(gen.CONFIGS[3])
+    cfg = gen.workload(gen.GQA_32K)
     shape = dataclasses.replace(gc.shape_of(cfg), window_mode=BAND)
-    print("config 3 band: generating", flush=True)
-    d = gen.generate_config(3, seed=0)
+    print("32k band: generating", flush=True)
+    d = gen.generate_workload(gen.GQA_32K, seed=0)
     g = gc.run_gpu(shape, d, keep_out_on_gpu=True)
     idx, qz = gc.check_select_quant(shape, d, g)
     rng = np.random.default_rng(34)
@@ -81,19 +81,19 @@ def test_band_config3_32k():
     assert mx <= gc.TOL_MAX and mean <= gc.TOL_MEAN
 
 
-@pytest.mark.parametrize("cfg_id", [1, 2])
-def test_final_chunk_matches_literal_algorithm(cfg_id):
+@pytest.mark.parametrize("name", [gen.SMALL, gen.GQA_8K])
+def test_final_chunk_matches_literal_algorithm(name):
     """The kernel's (fixed-window) rows of the final chunk [L-W, L) against
     Algorithm 2's Stage 3 taken literally (A and B unmasked, C causal,
     tile-by-tile online softmax), every head."""
-    cfg = gen.CONFIGS[cfg_id]
+    cfg = gen.workload(name)
     shape = gc.shape_of(cfg)
-    d = gen.generate_config(cfg_id, seed=0)
+    d = gen.generate_workload(name, seed=0)
     g = gc.run_gpu(shape, d)
     idx, qz = gc.check_select_quant(shape, d, g)
     Oc = orc.attention_final_chunk(d["Q"], d["K"], d["V"], shape.window, shape.bits_kv, idx, qz)
     P = shape.L - shape.window
     Og = g["out"].reshape(shape.B * shape.Hq, shape.L, 128)[:, P:]
     mx, mean = gc.attention_error(Og, Oc)
-    print(f"  config {cfg_id} final chunk: max-abs {mx:.3e} mean-abs {mean:.3e}", flush=True)
+    print(f"  {name} final chunk: max-abs {mx:.3e} mean-abs {mean:.3e}", flush=True)
     assert mx <= gc.TOL_MAX and mean <= gc.TOL_MEAN

@@ -102,7 +102,7 @@ def test_select_invariants_generated():
 def test_planted_lines_recovered():
     """Sanity: most planted vertical lines (aligned with the tail proxy) are
     found; the x10 outlier channels add score noise, so recall is not 1."""
-    d = gen.generate_config(1, seed=0)
+    d = gen.generate_workload(gen.SMALL, seed=0)
     idx, _ = orc.select_vertical(d["Q"], d["K"], 1, 64, 20000)
     planted = set(d["planted"][0].tolist())
     P = 960
