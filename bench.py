@@ -61,7 +61,8 @@ def attn_src_digest():
 
 
 def decode_src_digest():
-    return src_digest("decode.hip", "codes_dev.h", "quant_dev.h", "hyq_internal.h")
+    return src_digest("decode.hip", "decode_split.h", "codes_dev.h", "quant_dev.h",
+                      "hyq_internal.h")
 
 
 def load_traffic(workload, fname="attn_traffic.json", digest=None):

@@ -25,6 +25,7 @@
 // A workgroup (4 waves) merges its waves' states in LDS and writes one
 // partial (m, l, acc) per query head; a second kernel reduces the partials.
 #include "codes_dev.h"
+#include "decode_split.h"
 #include "hyq_internal.h"
 #include "quant_dev.h"
 
@@ -812,50 +813,17 @@ static int device_cus() {
   return n;
 }
 
-// Splits of the decode launch.  By default a wave takes about 32 KB of codes
-// (4 int4 or 2 8-bit blocks, as much as one full-precision tile).  The decode
-// loop is bound by each SIMD's vector ALU, so a launch takes about as long as
-// its busiest SIMD: (workgroups on the busiest CU) x (bytes of the busiest
-// wave).  When the default leaves the CUs unevenly loaded (312 workgroups on
-// 256 CUs: some CUs run two), the launch is reshaped to k workgroups per CU
-// with fewer, longer splits, and the full-precision tiles per wave chosen so
-// that no wave reads many more bytes than the others; the shape with the
-// smallest busiest-SIMD bytes wins.  Splits never exceed the default, which
-// bounds the workspace.
 DecodeSplit decode_split(const hyq_dcache& c) {
   DecodeSplit d;
   const int nbf = (c.n_frozen + kBlock - 1) / kBlock;
   d.nbq = nbf + c.n_merged;
-  const int u = c.bits_kv == 4 ? 4 : 2;
-  d.S_q = (d.nbq + kDecWaves * u - 1) / (kDecWaves * u);
   const int nft = (c.vl_rows + c.ring_rows) / kBlock;
-  d.S_f = (nft + kDecWaves - 1) / kDecWaves;
-  if (d.S_q == 0) return d;
-  const int64_t heads = (int64_t)c.B * c.Hkv;
-  const int64_t n_cu = device_cus();
-  const int64_t blk_bytes = 2 * kBlock * kHeadDim * c.bits_kv / 8;   // K and V codes
-  const int64_t tile_bytes = 2 * kBlock * kHeadDim * 2;              // K and V bf16 rows
-  auto wave_bytes = [&](int s_q, int s_f) {
-    const int64_t blks = (d.nbq + kDecWaves * s_q - 1) / ((int64_t)kDecWaves * s_q);
-    const int64_t tiles = s_f ? (nft + kDecWaves * s_f - 1) / ((int64_t)kDecWaves * s_f) : 0;
-    return std::max(blks * blk_bytes, tiles * tile_bytes);
-  };
-  const int64_t rounds = ((d.S_q + d.S_f) * heads + n_cu - 1) / n_cu;
-  int64_t best = rounds * wave_bytes(d.S_q, d.S_f);
-  for (int64_t k = 1; k < rounds && k <= 32; ++k) {
-    const int64_t fit = k * n_cu / heads;   // workgroups per KV head
-    for (int f = 1; f <= 4; ++f) {          // full-precision tiles per wave
-      const int s_f = (nft + kDecWaves * f - 1) / (kDecWaves * f);
-      const int s_q = (int)std::min<int64_t>(d.S_q, fit - s_f);
-      if (s_q < 1 || s_f > d.S_f) continue;
-      const int64_t cost = k * wave_bytes(s_q, s_f);
-      if (cost < best) {
-        best = cost;
-        d.S_q = s_q;
-        d.S_f = s_f;
-      }
-    }
-  }
+  const DecodeShape sh = choose_decode_split(
+      d.nbq, nft, (int64_t)c.B * c.Hkv, device_cus(), kDecWaves, c.bits_kv == 4 ? 4 : 2,
+      2 * kBlock * kHeadDim * c.bits_kv / 8,   // K and V codes of a block
+      2 * kBlock * kHeadDim * 2);              // K and V bf16 rows of a tile
+  d.S_q = sh.S_q;
+  d.S_f = sh.S_f;
   return d;
 }
 
