@@ -81,6 +81,25 @@ def load_traffic(workload, fname="attn_traffic.json", digest=None):
     return rec.get("hbm_bytes_per_launch")
 
 
+def host_identity():
+    """The host the CPU baseline ran on: CPUs this process may use, the
+    machine's CPU count and the CPU model string."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        affinity = None
+    return {"affinity_cpus": affinity, "os_cpu_count": os.cpu_count(), "cpu_model": model}
+
+
 def cpu_baseline(d, cfg, flops_total, budget_s):
     """The oracle (untuned) on a bounded sample: full selection and
     quantization of the layer, attention for a few heads x rows; the
@@ -89,9 +108,9 @@ def cpu_baseline(d, cfg, flops_total, budget_s):
     from oracle import hyq_oracle as orc
     try:
         from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:
-        cores = os.cpu_count() or 1
+        blas_threads = None
     L, W, D, Hq = cfg["L"], cfg["W"], 128, cfg["Hq"]
     t0 = time.perf_counter()
     idx, _ = orc.select_vertical(d["Q"], d["K"], cfg["Hkv"], W, cfg["budget_ppm"])
@@ -115,8 +134,13 @@ def cpu_baseline(d, cfg, flops_total, budget_s):
             break
         n_rows *= 2
     est = t_sel + t_quant + t_attn * (flops_total / f_attn)
+    host = host_identity()
+    # the oracle's attention is numpy matrix products (the BLAS thread pool);
+    # its selection and quantization run on one thread
+    cores = blas_threads or host["affinity_cpus"] or 1
     return {
         "value": flops_total / est / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+        "blas_threads": blas_threads, "host": host,
         "sample": (f"full selection ({t_sel:.2f} s) and quantization ({t_quant:.2f} s) of the layer; "
                    f"attention for {len(heads)} heads x {n_rows}-row random row sets "
                    f"({t_attn:.2f} s for {f_attn:.3e} FLOP); whole-layer time extrapolated "

@@ -112,3 +112,73 @@ def generate_workload(name: str, seed: int = 0, **overrides):
     data = generate(seed, WORKLOADS[name]["stream"], **cfg)
     data["cfg"] = cfg
     return data
+
+
+# bf16 bit patterns of the small integers the tie inputs use
+_BF16_POS_ZERO, _BF16_NEG_ZERO = np.uint16(0x0000), np.uint16(0x8000)
+_BF16_ONE, _BF16_MINUS_ONE = np.uint16(0x3F80), np.uint16(0xBF80)
+
+TIE_KINDS = ("positive", "signed_zero", "all_equal")
+
+
+def tie_inputs(seed: int, B: int, Hq: int, Hkv: int, L: int, W: int, k: int, kind: str,
+               D: int = 128):
+    """Integer-valued bf16 inputs whose selection scores tie at the k-th
+    largest value, spread over the whole prefix [0, P), P = L - W.
+
+    Q entries are drawn from {-1, 0, +1}, so the summed tail queries of a
+    KV head are an integer vector c (computed here in int64 to build K; the
+    tested paths compute it in float32, where it is exact).  Each prefix key
+    row is one of a few patterns whose scores against c are known exactly:
+      top    sign(c)                      score sum |c_d|
+      mid    sign(c) on channels < D/2    score sum_{d < D/2} |c_d| (< top)
+      +0     all +0.0                     score +0
+      -0     -0.0 where c_d >= 0, +0.0 where c_d < 0 (every product -0)
+                                          score -0
+      neg    -sign(c)                     score -sum |c_d|
+    kind = "positive": k // 3 top rows, 8k mid rows (the k-th largest is the
+    mid score: many more ties than the rows still to take), the rest +0, -0
+    and neg rows.  kind = "signed_zero": k // 2 top rows, 4k zero rows (+0 and
+    -0 alternating by draw), the rest neg (the threshold is zero).
+    kind = "all_equal": every tail query row is 0, so every score is a zero.
+    Window rows and V are standard-normal bf16.  Returns dict(Q, K, V)."""
+    if kind not in TIE_KINDS:
+        raise ValueError(f"kind must be one of {TIE_KINDS}")
+    g = Hq // Hkv
+    P = max(0, L - W)
+    t = min(max(W, 1), L)
+    rng = np.random.default_rng([int(seed), 7000 + TIE_KINDS.index(kind)])
+    pick = rng.integers(-1, 2, size=(B, Hq, L, D))
+    Q = np.where(pick > 0, _BF16_ONE, np.where(pick < 0, _BF16_MINUS_ONE, _BF16_POS_ZERO))
+    Q = Q.astype(np.uint16)
+    if kind == "all_equal":
+        Q[:, :, L - t:, :] = _BF16_POS_ZERO
+    K = f32_to_bf16_bits(rng.standard_normal((B, Hkv, L, D), dtype=np.float32))
+    V = f32_to_bf16_bits(rng.standard_normal((B, Hkv, L, D), dtype=np.float32))
+    for b in range(B):
+        for j in range(Hkv):
+            c = pick[b, j * g:(j + 1) * g, L - t:, :].sum(axis=(0, 1)) if kind != "all_equal" \
+                else np.zeros(D, dtype=np.int64)
+            top = np.where(c > 0, _BF16_ONE, np.where(c < 0, _BF16_MINUS_ONE, _BF16_POS_ZERO))
+            mid = top.copy()
+            mid[D // 2:] = _BF16_POS_ZERO
+            neg = np.where(c > 0, _BF16_MINUS_ONE, np.where(c < 0, _BF16_ONE, _BF16_POS_ZERO))
+            pz = np.full(D, _BF16_POS_ZERO, dtype=np.uint16)
+            nz = np.where(c >= 0, _BF16_NEG_ZERO, _BF16_POS_ZERO)
+            pats = np.stack([top, mid, pz, nz, neg]).astype(np.uint16)
+            order = rng.permutation(P)
+            which = np.empty(P, dtype=np.int64)
+            if kind == "positive":
+                n_top, n_mid = min(P, k // 3), min(P - min(P, k // 3), 8 * k)
+                which[order[:n_top]] = 0
+                which[order[n_top:n_top + n_mid]] = 1
+                which[order[n_top + n_mid:]] = rng.choice([2, 3, 4], size=P - n_top - n_mid)
+            elif kind == "signed_zero":
+                n_top, n_zero = min(P, k // 2), min(P - min(P, k // 2), 4 * k)
+                which[order[:n_top]] = 0
+                which[order[n_top:n_top + n_zero]] = rng.choice([2, 3], size=n_zero)
+                which[order[n_top + n_zero:]] = 4
+            else:
+                which[:] = rng.choice([2, 3], size=P)
+            K[b, j, :P, :] = pats[which]
+    return dict(Q=Q, K=K, V=V)

@@ -124,3 +124,36 @@ def test_pinned_tree_order_matters():
     v = np.array([[1e8, 1.0, -1e8, 1.0]], dtype=np.float32)
     # (v0 + v2) + (v1 + v3) = 0 + 2 = 2
     assert orc.fold_sum(v)[0] == np.float32(2.0)
+
+
+@pytest.mark.parametrize("kind", gen.TIE_KINDS)
+def test_tie_inputs_tie_at_threshold(kind):
+    """The tie inputs (used by the GPU tie test) really put many exact ties,
+    and signed zeros, at the k-th largest score, spread over the prefix; on
+    them the oracle's selection equals int64 scores ranked by rank counting
+    with -0 == +0 (lowest position wins)."""
+    B, Hq, Hkv, L, W, ppm = 1, 8, 4, 2048, 64, 20000
+    k = orc.sizes(L, W, ppm)["k"]
+    P = L - W
+    d = gen.tie_inputs(11, B, Hq, Hkv, L, W, k, kind)
+    idx, S = orc.select_vertical(d["Q"], d["K"], Hkv, W, ppm)
+    Qi = gen.bf16_bits_to_f32(d["Q"]).astype(np.int64)
+    Ki = gen.bf16_bits_to_f32(d["K"]).astype(np.int64)
+    g = Hq // Hkv
+    for j in range(Hkv):
+        c = Qi[0, j * g:(j + 1) * g, L - W:, :].sum(axis=(0, 1))
+        Sint = Ki[0, j, :P] @ c
+        np.testing.assert_array_equal(S[0, j], Sint.astype(np.float32))
+        T = np.sort(Sint)[::-1][k - 1]
+        n_gt, n_eq = int((Sint > T).sum()), int((Sint == T).sum())
+        assert n_eq > k - n_gt >= 1                   # ties at the threshold must be split
+        eq_pos = np.nonzero(Sint == T)[0]
+        assert eq_pos.min() < P // 8 and eq_pos.max() > P - P // 8
+        if kind != "positive":
+            assert T == 0
+            bits = S[0, j].view(np.uint32)
+            zero_pos = np.nonzero(Sint == 0)[0]
+            assert np.any(bits[zero_pos] == 0x80000000) and np.any(bits[zero_pos] == 0)
+        # rank counting: p is chosen iff fewer than k keys beat it
+        beat = np.array([(Sint > Sint[p]).sum() + (Sint[:p] == Sint[p]).sum() for p in range(P)])
+        np.testing.assert_array_equal(idx[0, j], np.nonzero(beat < k)[0])
