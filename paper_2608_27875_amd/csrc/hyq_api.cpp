@@ -101,11 +101,38 @@ int check_shape(const hyq_shape* s, hyq_sizes* z) {
     z->v_codes_bytes = B * Hkv * (size_t)z->n_kvblk * D * (size_t)(bs * s->bits_kv / 8);
     z->kv_scale_bytes = B * Hkv * (size_t)z->n_kvblk * 4;
   }
-  z->select_ws_bytes = k > 0 ? align256(B * Hkv * D * 4) + align256(z->scores_bytes) +
+  z->select_ws_bytes = k > 0 ? align256(B * Hq * D * 4) + align256(z->scores_bytes) +
+                                   align256(B * Hkv * hyq::kSelHistBins * 4) +
+                                   align256(hyq::select_topk_ws_bytes((int)(B * Hkv), (int)P)) +
                                    (s->selector == HYQ_SEL_COLMASS
                                         ? align256(hyq::colmass_ws_bytes(*s)) : 0)
                              : 0;
   return HYQ_OK;
+}
+
+// The selection workspace: per-head tail sums [B][Hq][D], the scores
+// [B][Hkv][P] (unused when the caller passes its own), the top-k key
+// histogram, the top-k candidates and bitmaps, the column mass's scratch.
+struct SelectWs {
+  float* qsum;
+  float* scores;
+  uint32_t* hist;
+  uint32_t* tws;
+  float* cm;
+};
+SelectWs select_ws(const hyq_shape& s, const hyq_sizes& z, void* ws, float* scores_out) {
+  char* p = static_cast<char*>(ws);
+  SelectWs r;
+  r.qsum = reinterpret_cast<float*>(p);
+  p += align256((size_t)s.B * s.Hq * s.D * 4);
+  r.scores = scores_out ? scores_out : reinterpret_cast<float*>(p);
+  p += align256(z.scores_bytes);
+  r.hist = reinterpret_cast<uint32_t*>(p);
+  p += align256((size_t)s.B * s.Hkv * hyq::kSelHistBins * 4);
+  r.tws = reinterpret_cast<uint32_t*>(p);
+  p += align256(hyq::select_topk_ws_bytes(s.B * s.Hkv, z.P));
+  r.cm = reinterpret_cast<float*>(p);
+  return r;
 }
 
 int64_t round_up64(int64_t x) { return (x + 63) / 64 * 64; }
@@ -234,14 +261,10 @@ HYQ_API int hyq_select_vertical(const hyq_shape* shape, const void* Q, const voi
   if (!ws || ws_bytes < z.select_ws_bytes)
     return fail(HYQ_EINVAL, "workspace too small: %zu bytes given, %zu needed", ws_bytes,
                 z.select_ws_bytes);
-  float* qsum = static_cast<float*>(ws);
-  const size_t off_sc = align256((size_t)shape->B * shape->Hkv * shape->D * 4);
-  float* sc = scores ? scores : reinterpret_cast<float*>(static_cast<char*>(ws) + off_sc);
-  float* cm = reinterpret_cast<float*>(static_cast<char*>(ws) + off_sc +
-                                       align256(z.scores_bytes));
+  const SelectWs w = select_ws(*shape, z, ws, scores);
   return hip_status(hyq::launch_select(*shape, z, static_cast<const uint16_t*>(Q),
-                                       static_cast<const uint16_t*>(K), idx, sc, qsum, cm,
-                                       static_cast<hipStream_t>(stream)),
+                                       static_cast<const uint16_t*>(K), idx, w.scores, w.qsum,
+                                       w.hist, w.tws, w.cm, static_cast<hipStream_t>(stream)),
                     "hyq_select_vertical launch");
 }
 
@@ -332,14 +355,10 @@ HYQ_API int hyq_freeze(const hyq_shape* prefill, const void* Q, const void* K, c
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int BHkv = prefill->B * prefill->Hkv;
   if (z.k > 0) {
-    float* qsum = static_cast<float*>(ws);
-    const size_t off_sc = align256((size_t)BHkv * prefill->D * 4);
-    float* sc = reinterpret_cast<float*>(static_cast<char*>(ws) + off_sc);
-    float* cm = reinterpret_cast<float*>(static_cast<char*>(ws) + off_sc +
-                                         align256(z.scores_bytes));
+    const SelectWs w = select_ws(*prefill, z, ws, nullptr);
     hipError_t e = hyq::launch_select(*prefill, z, static_cast<const uint16_t*>(Q),
-                                      static_cast<const uint16_t*>(K), cache->vl_pos, sc, qsum,
-                                      cm, st);
+                                      static_cast<const uint16_t*>(K), cache->vl_pos, w.scores,
+                                      w.qsum, w.hist, w.tws, w.cm, st);
     if (e != hipSuccess) return hip_status(e, "hyq_freeze selection launch");
   }
   if (cache->cap_blocks > 0) {

@@ -12,9 +12,15 @@ namespace hyq {
 
 // ---- host-side launch wrappers (each returns a hipError_t) ----------------
 
+// Selection (Algorithm 1, or the column mass) into idx.  Scratch: scores
+// ([B][Hkv][P], may be the caller's output), qsum (the per-head tail sums,
+// [B][Hq][D]), hist ([B][Hkv][kSelHistBins] key counts), tws
+// (select_topk_ws_bytes of top-k candidates and bitmaps), cm_ws (the column
+// mass's scratch).
+size_t select_topk_ws_bytes(int BH, int P);
 hipError_t launch_select(const hyq_shape& s, const hyq_sizes& z, const uint16_t* Q,
                          const uint16_t* K, int32_t* idx, float* scores, float* qsum,
-                         float* cm_ws, hipStream_t st);
+                         uint32_t* hist, uint32_t* tws, float* cm_ws, hipStream_t st);
 
 // Column-mass scores (eq. vl_score) into scores[B][Hkv][P]; cm_ws holds
 // colmass_ws_bytes(s) bytes of scratch.
@@ -73,5 +79,8 @@ __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w 
 
 constexpr int kHeadDim = 128;
 constexpr int kBlock = 64;
+// Top-k key histogram: bins of the top kSelHistBits bits of the score order key.
+constexpr int kSelHistBits = 12;
+constexpr int kSelHistBins = 1 << kSelHistBits;
 
 }  // namespace hyq

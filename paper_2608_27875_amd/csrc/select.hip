@@ -11,6 +11,22 @@
 // Every floating-point operation here is a separately rounded float32
 // add or multiply in a fixed order, so the result is reproducible bit for
 // bit; contraction into fused multiply-adds is disabled for this file.
+//
+// The top-k works on order keys (an order-preserving map of the float
+// scores to uint32):
+//   - while the scores are produced, every workgroup counts its keys by
+//     their top 12 bits in LDS and adds the non-empty bins to a histogram of
+//     its KV head in the workspace;
+//   - the classification kernel (1024 keys per workgroup) finds the bin
+//     holding the k-th largest key from that histogram, writes a bitmap of
+//     the positions in higher bins and appends the keys of that bin (about
+//     1% of them) to a candidate list;
+//   - one workgroup per KV head resolves the remaining 20 bits of the
+//     threshold with two 10-bit radix passes over the candidates, then
+//     writes the chosen positions in ascending order (ordered compaction of
+//     the bitmaps; keys equal to the threshold lowest position first).
+// The per-key work runs on many workgroups; the one workgroup per head
+// touches only the candidates and one bitmap word per 32 positions.
 #include "hyq_internal.h"
 
 #pragma clang fp contract(off)
@@ -18,81 +34,7 @@
 namespace hyq {
 namespace {
 
-constexpr int kTailBatch = 32;
-
-// One workgroup per (b, j); thread (r, d) owns query head j*g + r and
-// channel d.  Each thread adds its t tail values in ascending row order
-// from +0 (loads are issued a batch at a time to hide latency); then the
-// g per-head sums are added in head order.
-__global__ void __launch_bounds__(1024)
-tail_proxy_kernel(const uint16_t* __restrict__ Q, float* __restrict__ qsum,
-                  int Hq, int Hkv, int L, int t) {
-  extern __shared__ float part[];  // [g][D]
-  const int g = Hq / Hkv;
-  const int bj = blockIdx.x;
-  const int b = bj / Hkv, j = bj % Hkv;
-  const int r = threadIdx.x / kHeadDim, d = threadIdx.x % kHeadDim;
-  const uint16_t* q = Q + ((size_t)(b * Hq + j * g + r) * L + (L - t)) * kHeadDim + d;
-  float a = 0.0f;
-  int i = 0;
-  for (; i + kTailBatch <= t; i += kTailBatch) {
-    uint32_t v[kTailBatch];
-#pragma unroll
-    for (int u = 0; u < kTailBatch; ++u) v[u] = q[(size_t)(i + u) * kHeadDim];
-#pragma unroll
-    for (int u = 0; u < kTailBatch; ++u) a = a + bf16_bits_to_f32(v[u]);
-  }
-  for (; i < t; ++i) a = a + bf16_bits_to_f32(q[(size_t)i * kHeadDim]);
-  part[r * kHeadDim + d] = a;
-  __syncthreads();
-  if (r == 0) {
-    float s = part[d];
-    for (int rr = 1; rr < g; ++rr) s = s + part[rr * kHeadDim + d];
-    qsum[(size_t)bj * kHeadDim + d] = s;
-  }
-}
-
-// One thread per prefix key: products qsum[d] * K[p][d] rounded separately,
-// then v[l] = prod[l] + prod[l + 64] and repeated halving 32 .. 1.
-__global__ void __launch_bounds__(256)
-score_kernel(const uint16_t* __restrict__ K, const float* __restrict__ qsum,
-             float* __restrict__ S, int L, int P) {
-  __shared__ float qs[kHeadDim];
-  const int bj = blockIdx.y;
-  if (threadIdx.x < kHeadDim) qs[threadIdx.x] = qsum[(size_t)bj * kHeadDim + threadIdx.x];
-  __syncthreads();
-  const int p = blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= P) return;
-  const uint4* row = reinterpret_cast<const uint4*>(K + ((size_t)bj * L + p) * kHeadDim);
-  uint4 lo[8], hi[8];
-#pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    lo[u] = row[u];       // channels 0..63
-    hi[u] = row[u + 8];   // channels 64..127
-  }
-  float v[64];
-#pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const uint32_t wl[4] = {lo[u].x, lo[u].y, lo[u].z, lo[u].w};
-    const uint32_t wh[4] = {hi[u].x, hi[u].y, hi[u].z, hi[u].w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int l0 = u * 8 + e * 2;
-      const float p0 = qs[l0] * bf16_lo(wl[e]);
-      const float p1 = qs[l0 + 1] * bf16_hi(wl[e]);
-      const float h0 = qs[l0 + 64] * bf16_lo(wh[e]);
-      const float h1 = qs[l0 + 65] * bf16_hi(wh[e]);
-      v[l0] = p0 + h0;
-      v[l0 + 1] = p1 + h1;
-    }
-  }
-#pragma unroll
-  for (int h = 32; h >= 1; h >>= 1) {
-#pragma unroll
-    for (int l = 0; l < h; ++l) v[l] = v[l] + v[l + h];
-  }
-  S[(size_t)bj * P + p] = v[0];
-}
+constexpr int kHistShift = 32 - kSelHistBits;   // the histogram bin is key >> kHistShift
 
 // Order-preserving map float -> uint32 (larger float, larger key); -0 -> +0.
 __device__ __forceinline__ uint32_t order_key(float f) {
@@ -100,139 +42,482 @@ __device__ __forceinline__ uint32_t order_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-constexpr int kTopkThreads = 1024;
-constexpr int kTopkWaves = kTopkThreads / 64;
+// Per-head top-k scratch in the workspace: a 4-word header (the candidate
+// count, then the bin of the k-th largest key and the keys still to take in
+// it, as the classification finds them), the candidate list ((key, position) of the keys in the
+// threshold's bin, at most P of them) and the bitmap of positions in higher
+// bins (an even number of words).
+__host__ __device__ __forceinline__ size_t topk_ws_words(int P) {
+  return 4 + 2 * (size_t)P + (size_t)(P + 63) / 64 * 2;
+}
+struct TopkWs {
+  uint32_t* ncand;   // header: [0] candidates, [1] bin, [2] keys of the bin to take
+  uint2* cand;
+  uint32_t* gt;
+};
+__device__ __forceinline__ TopkWs topk_ws(uint32_t* base, int bj, int P) {
+  uint32_t* h = base + (size_t)bj * topk_ws_words(P);
+  TopkWs w;
+  w.ncand = h;
+  w.cand = reinterpret_cast<uint2*>(h + 4);
+  w.gt = h + 4 + 2 * (size_t)P;
+  return w;
+}
 
-// One workgroup per (b, j).  Radix select over the 32-bit order keys, 8 bits
-// per pass (per-wave LDS histograms), finds the k-th largest key T and how
-// many keys equal to T are taken (the lowest positions).  Then an ordered
-// compaction writes the chosen positions ascending (below).
-__global__ void __launch_bounds__(kTopkThreads)
-topk_kernel(const float* __restrict__ S, int32_t* __restrict__ idx, int P, int k) {
-  __shared__ uint32_t hist[kTopkWaves][256];
-  __shared__ int w_gt[kTopkWaves], w_eq[kTopkWaves];
-  __shared__ uint32_t sh_digit;
-  __shared__ int sh_remaining;
-  const int bj = blockIdx.x;
-  const float* s = S + (size_t)bj * P;
+// One workgroup per (b, h).  The head's t tail rows are staged through LDS
+// kTailRows at a time (each of the 4 row groups of threads loads a quarter,
+// all loads in flight at once); then thread d adds the staged values of
+// channel d in ascending row order, continuing from +0 over all t rows, which
+// gives qpart[b][h][d].  The score kernel adds the g heads of a group in head
+// order.  The first head of each group also clears the key histogram and
+// the top-k candidate count of its (b, j), which the next kernels fill.
+constexpr int kTailRows = 256;
+constexpr int kTailThreads = 4 * kHeadDim;
+__global__ void __launch_bounds__(kTailThreads)
+tail_proxy_kernel(const uint16_t* __restrict__ Q, float* __restrict__ qpart,
+                  uint32_t* __restrict__ hist, uint32_t* __restrict__ tws, int Hq, int Hkv, int L,
+                  int t, int P) {
+  __shared__ uint16_t rows[kTailRows][kHeadDim];
+  const int g = Hq / Hkv;
+  const int bh = blockIdx.x;
+  const int d = threadIdx.x % kHeadDim, qr = threadIdx.x / kHeadDim;
+  if (bh % g == 0) {
+    uint32_t* hj = hist + (size_t)(bh / g) * kSelHistBins;
+    for (int i = threadIdx.x; i < kSelHistBins; i += kTailThreads) hj[i] = 0u;
+    if (threadIdx.x == 0) tws[(size_t)(bh / g) * topk_ws_words(P)] = 0u;
+  }
+  const uint16_t* q = Q + ((size_t)bh * L + (L - t)) * kHeadDim + d;
+  constexpr int kPer = kTailRows / 4;
+  float a = 0.0f;
+  for (int r0 = 0; r0 < t; r0 += kTailRows) {
+    const int n = min(kTailRows, t - r0);
+    uint16_t v[kPer];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u)   // rows past the tail re-read its last row (never added)
+      v[u] = q[(size_t)min(r0 + qr * kPer + u, t - 1) * kHeadDim];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) rows[qr * kPer + u][d] = v[u];
+    __syncthreads();
+    if (qr == 0) {
+      for (int i0 = 0; i0 < n; i0 += 32) {   // 32 LDS reads in flight, then the adds in order
+        uint16_t x[32];
+#pragma unroll
+        for (int i = 0; i < 32; ++i) x[i] = rows[min(i0 + i, kTailRows - 1)][d];
+#pragma unroll
+        for (int i = 0; i < 32; ++i)
+          if (i0 + i < n) a = a + bf16_bits_to_f32(x[i]);
+      }
+    }
+    __syncthreads();
+  }
+  if (qr == 0) qpart[(size_t)bh * kHeadDim + d] = a;
+}
+
+// Workgroup-local key histogram (top kSelHistBits bits of the order key),
+// flushed into the KV head's histogram in global memory.
+constexpr int kHistThreads = 1024;
+constexpr int kScoreRows = kHistThreads;   // keys per workgroup (one per thread)
+
+__device__ __forceinline__ void hist_clear(uint32_t* lh) {
+  for (int i = threadIdx.x; i < kSelHistBins; i += blockDim.x) lh[i] = 0u;
+}
+__device__ __forceinline__ void hist_flush(const uint32_t* lh, uint32_t* __restrict__ gh) {
+  for (int i = threadIdx.x; i < kSelHistBins; i += blockDim.x) {
+    const uint32_t c = lh[i];
+    if (c) atomicAdd(gh + i, c);
+  }
+}
+
+// Lane exchange within groups of four lanes (DPP quad permutations).
+__device__ __forceinline__ float xor1(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float xor2(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xF, 0xF, true));
+}
+
+// Scores of 1024 prefix keys per workgroup, 64 per wave.  A key row is read
+// by 4 lanes: lane c (0..3) of the row's group loads the 16-byte chunks c,
+// c+4, c+8, c+12 (channels 8c.., 32+8c.., 64+8c.., 96+8c.., eight each), so
+// one load instruction covers 16 rows, 64 contiguous bytes each.  The pinned
+// fold then runs as a butterfly: the halving steps l + 64 and l + 32 are
+// in-lane, steps 16 and 8 pair lane c with lane c^2 and c^1 (the lower lane
+// of a pair holds v[l], its partner v[l + h]; float addition is
+// commutative, so both lanes get the bits of v[l] + v[l + h]), and steps
+// 4, 2, 1 are in-lane again.
+__global__ void __launch_bounds__(kHistThreads)
+score_kernel(const uint16_t* __restrict__ K, const float* __restrict__ qpart,
+             float* __restrict__ S, uint32_t* __restrict__ hist, int g, int L, int P) {
+  __shared__ uint32_t lh[kSelHistBins];
+  __shared__ float4 qs[kHeadDim / 4];
+  const int bj = blockIdx.x;   // consecutive workgroups take consecutive heads (see the launch)
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-
-  uint32_t prefix = 0, mask = 0;
-  int remaining = k;  // how many of the keys matching `prefix` are still to take
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int i = threadIdx.x; i < kTopkWaves * 256; i += kTopkThreads) (&hist[0][0])[i] = 0;
-    __syncthreads();
-    for (int p = threadIdx.x; p < P; p += kTopkThreads) {
-      const uint32_t u = order_key(s[p]);
-      if ((u & mask) == prefix) atomicAdd(&hist[w][(u >> shift) & 255u], 1u);
-    }
-    __syncthreads();
-    if (w == 0) {
-      // lane owns bins 4*lane .. 4*lane+3; suffix sums from the top bin down
-      uint32_t c[4];
-      uint32_t mine = 0;
+  const int c = lane & 3, rsub = lane >> 2;
+  const int base = blockIdx.y * kScoreRows + w * 64;
+  const uint4* Kb = reinterpret_cast<const uint4*>(K + (size_t)bj * L * kHeadDim);
+  uint4 kr[4][4];   // [iteration][quarter q]: chunk c + 4q of row base + 16*it + rsub
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        uint32_t t = 0;
-        for (int ww = 0; ww < kTopkWaves; ++ww) t += hist[ww][4 * lane + e];
-        c[e] = t;
-        mine += t;
-      }
-      // inclusive suffix sum over lanes: above[lane] = sum of bins >= 4*lane
-      uint32_t suf = mine;
+  for (int it = 0; it < 4; ++it) {
+    // rows past P load row P-1 (unconditional loads stay in flight together);
+    // their scores are never stored
+    const uint4* rp = Kb + (size_t)min(base + it * 16 + rsub, P - 1) * (kHeadDim / 8);
 #pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t y = __shfl_down(suf, o, 64);
-        if (lane + o < 64) suf += y;
-      }
-      const uint32_t above_lane = suf - mine;   // count in bins > 4*lane+3
-      // the digit is in this lane's bins if above_lane < remaining <= suf
-      if (above_lane < (uint32_t)remaining && (uint32_t)remaining <= suf) {
-        uint32_t acc = above_lane;
-        for (int e = 3; e >= 0; --e) {
-          if (acc + c[e] >= (uint32_t)remaining) {
-            sh_digit = 4 * lane + e;
-            sh_remaining = remaining - (int)acc;
-            break;
-          }
-          acc += c[e];
-        }
-      }
-    }
-    __syncthreads();
-    prefix |= sh_digit << shift;
-    mask |= 255u << shift;
-    remaining = sh_remaining;
-    __syncthreads();
+    for (int q = 0; q < 4; ++q) kr[it][q] = rp[c + 4 * q];
   }
-  const uint32_t T = prefix;
-  const int need_eq = remaining;  // keys equal to T to take, lowest positions first
-
-  // Ordered compaction: wave w owns positions [w*R, (w+1)*R) and reads them
-  // 64 at a time (coalesced); a first sweep counts its keys above and equal to
-  // T, the wave totals give each wave its output offset and its share of the
-  // keys equal to T, a second sweep writes the positions in order.
-  const int R = ((P + kTopkWaves - 1) / kTopkWaves + 63) & ~63;
-  const int q0 = min(P, w * R), q1 = min(P, q0 + R);
-  int gtc = 0, eqc = 0;   // wave-uniform
-  for (int b = q0; b < q1; b += 64) {
-    const int p = b + lane;
-    const uint32_t u = p < q1 ? order_key(s[p]) : 0u;
-    gtc += (int)__popcll(__ballot(p < q1 && u > T));
-    eqc += (int)__popcll(__ballot(p < q1 && u == T));
-  }
-  if (lane == 0) {
-    w_gt[w] = gtc;
-    w_eq[w] = eqc;
+  hist_clear(lh);
+  if (threadIdx.x < kHeadDim) {   // qsum = the g head partials added in head order
+    const float* pp = qpart + (size_t)bj * g * kHeadDim + threadIdx.x;
+    float part[8];   // g <= 8; unconditional loads, all in flight
+#pragma unroll
+    for (int r = 0; r < 8; ++r) part[r] = pp[(size_t)min(r, g - 1) * kHeadDim];
+    float a = part[0];
+#pragma unroll
+    for (int r = 1; r < 8; ++r)
+      if (r < g) a = a + part[r];
+    reinterpret_cast<float*>(qs)[threadIdx.x] = a;
   }
   __syncthreads();
-  int o = 0, eq_before = 0;
-  for (int v = 0; v < w; ++v) {
-    o += w_gt[v] + max(0, min(w_eq[v], need_eq - eq_before));
-    eq_before += w_eq[v];
+  // qv[q][e] = qsum[32q + 8c + e]
+  float qv[4][8];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float4 a = qs[8 * q + 2 * c], b = qs[8 * q + 2 * c + 1];
+    qv[q][0] = a.x; qv[q][1] = a.y; qv[q][2] = a.z; qv[q][3] = a.w;
+    qv[q][4] = b.x; qv[q][5] = b.y; qv[q][6] = b.z; qv[q][7] = b.w;
   }
-  const int take_eq = max(0, min(eqc, need_eq - eq_before));
-  int32_t* out = idx + (size_t)bj * k;
-  int eq_seen = 0;
-  for (int b = q0; b < q1; b += 64) {
-    const int p = b + lane;
-    const bool in = p < q1;
-    const uint32_t u = in ? order_key(s[p]) : 0u;
-    const bool is_eq = in && u == T;
-    const uint64_t meq = __ballot(is_eq);
-    const int eq_rank = eq_seen + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(meq >> 32),
-                                      __builtin_amdgcn_mbcnt_lo((uint32_t)meq, 0u));
-    const bool sel = in && (u > T || (is_eq && eq_rank < take_eq));
-    const uint64_t msel = __ballot(sel);
-    if (sel) {
-      const int pos = o + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(msel >> 32),
-                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)msel, 0u));
-      if (pos < k) out[pos] = p;   // never more than k (guards a malformed threshold)
+
+  float sv[4];
+#pragma unroll
+  for (int it = 0; it < 4; ++it) {
+    float pr[4][8];   // products of channel 32q + 8c + e
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t wq[4] = {kr[it][q].x, kr[it][q].y, kr[it][q].z, kr[it][q].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        pr[q][2 * e] = qv[q][2 * e] * bf16_lo(wq[e]);
+        pr[q][2 * e + 1] = qv[q][2 * e + 1] * bf16_hi(wq[e]);
+      }
     }
-    o += (int)__popcll(msel);
-    eq_seen += (int)__popcll(meq);
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float a = pr[0][e] + pr[2][e];   // step 64: l = 8c+e,    l + 64
+      const float b = pr[1][e] + pr[3][e];   //          l = 32+8c+e, l + 64
+      v[e] = a + b;                          // step 32: l = 8c+e,    l + 32
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v[e] + xor2(v[e]);   // step 16
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = v[e] + xor1(v[e]);   // step 8
+#pragma unroll
+    for (int h = 4; h >= 1; h >>= 1)
+#pragma unroll
+      for (int e = 0; e < h; ++e) v[e] = v[e] + v[e + h];
+    sv[it] = v[0];
+  }
+  // lane l takes the score of row base + l: iteration l/16, row group l%16
+  float s = 0.0f;
+#pragma unroll
+  for (int it = 0; it < 4; ++it) {
+    const float x = __shfl(sv[it], 4 * (lane & 15), 64);
+    if ((lane >> 4) == it) s = x;
+  }
+  const int p = base + lane;
+  if (p < P) {
+    S[(size_t)bj * P + p] = s;
+    atomicAdd(&lh[order_key(s) >> kHistShift], 1u);
+  }
+  __syncthreads();
+  hist_flush(lh, hist + (size_t)bj * kSelHistBins);
+}
+
+// Clears the key histogram and the top-k candidate count of each head (one
+// workgroup per head; the tail-proxy kernel does this on the other path).
+__global__ void hist_zero_kernel(uint32_t* __restrict__ hist, uint32_t* __restrict__ tws, int P) {
+  const int bj = blockIdx.x;
+  for (int i = threadIdx.x; i < kSelHistBins; i += blockDim.x)
+    hist[(size_t)bj * kSelHistBins + i] = 0u;
+  if (threadIdx.x == 0) tws[(size_t)bj * topk_ws_words(P)] = 0u;
+}
+
+// Key histogram of scores computed elsewhere (the column-mass selector).
+__global__ void __launch_bounds__(kHistThreads)
+hist_kernel(const float* __restrict__ S, uint32_t* __restrict__ hist, int P) {
+  __shared__ uint32_t lh[kSelHistBins];
+  const int bj = blockIdx.x;
+  hist_clear(lh);
+  __syncthreads();
+  const int p = blockIdx.y * kScoreRows + threadIdx.x;
+  if (p < P) atomicAdd(&lh[order_key(S[(size_t)bj * P + p]) >> kHistShift], 1u);
+  __syncthreads();
+  hist_flush(lh, hist + (size_t)bj * kSelHistBins);
+}
+
+constexpr int kTopkThreads = 1024;
+constexpr int kTopkWaves = kTopkThreads / 64;
+constexpr int kDigitBits = 10;
+constexpr int kDigitBins = 1 << kDigitBits;
+static_assert(kSelHistBits + 2 * kDigitBits == 32, "bin + two digits cover the key");
+static_assert(kSelHistBins == 4 * kTopkThreads, "four histogram bins per thread");
+static_assert(kDigitBins == kTopkThreads, "one digit bin per thread");
+
+struct TopkShared {
+  uint32_t dig[kDigitBins];
+  uint32_t wtot[kTopkWaves];
+  uint32_t sel_bin;
+  int sel_rem;
+};
+
+// Inclusive suffix sum over the workgroup's threads in thread order: the
+// sum of x over this thread and every later one.
+__device__ __forceinline__ uint32_t block_suffix(uint32_t x, TopkShared& sh) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  uint32_t s = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_down(s, o, 64);
+    if (lane + o < 64) s += y;
+  }
+  if (lane == 0) sh.wtot[w] = s;
+  __syncthreads();
+  uint32_t later = 0;
+  for (int v = w + 1; v < kTopkWaves; ++v) later += sh.wtot[v];
+  __syncthreads();
+  return s + later;
+}
+
+// Exclusive prefix sum over the workgroup's threads in thread order; the
+// sum over all threads goes to `total`.
+__device__ __forceinline__ uint32_t block_prefix_excl(uint32_t x, TopkShared& sh,
+                                                      uint32_t& total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  uint32_t s = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(s, o, 64);
+    if (lane >= o) s += y;
+  }
+  if (lane == 63) sh.wtot[w] = s;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+  for (int v = 0; v < kTopkWaves; ++v) {
+    const uint32_t t = sh.wtot[v];
+    before += v < w ? t : 0u;
+    all += t;
+  }
+  __syncthreads();
+  total = all;
+  return before + s - x;
+}
+
+// Thread t owns the n bins c[0..n) = bins n*t .. n*t+n-1 of an ascending
+// histogram.  Finds the bin holding the need-th largest key and how many
+// keys of that bin are still to take; the owning thread publishes both.
+template <int N>
+__device__ __forceinline__ void find_bin(const uint32_t (&c)[N], int need, TopkShared& sh) {
+  uint32_t mine = 0;
+#pragma unroll
+  for (int e = 0; e < N; ++e) mine += c[e];
+  const uint32_t suf = block_suffix(mine, sh);
+  const uint32_t above = suf - mine;   // keys in the bins of later threads
+  if (above < (uint32_t)need && (uint32_t)need <= suf) {
+    uint32_t acc = above;
+#pragma unroll
+    for (int e = N - 1; e >= 0; --e) {
+      if (acc + c[e] >= (uint32_t)need) {
+        sh.sel_bin = (uint32_t)(N * threadIdx.x + e);
+        sh.sel_rem = need - (int)acc;
+        break;
+      }
+      acc += c[e];
+    }
+  }
+  __syncthreads();
+}
+
+// The bin of the k-th largest key of head bj from its histogram.
+__device__ __forceinline__ void hist_bin(const uint32_t* __restrict__ hist, int bj, int k,
+                                         TopkShared& sh) {
+  const uint4 h4 = reinterpret_cast<const uint4*>(hist + (size_t)bj * kSelHistBins)[threadIdx.x];
+  const uint32_t hc[4] = {h4.x, h4.y, h4.z, h4.w};
+  find_bin<4>(hc, k, sh);
+}
+
+// Classification, 1024 keys per workgroup (grid: head fastest, then key
+// chunk; one key per thread, coalesced): every workgroup finds the bin of
+// the k-th largest key from the histogram; a ballot per wave gives the 64
+// positions' bits "in a higher bin" as two bitmap words; the keys of that
+// bin are appended to the head's candidate list (one atomic reservation per
+// wave).
+__global__ void __launch_bounds__(kTopkThreads)
+topk_classify_kernel(const float* __restrict__ S, const uint32_t* __restrict__ hist,
+                     uint32_t* __restrict__ tws, int P, int k) {
+  __shared__ TopkShared sh;
+  const int bj = blockIdx.x;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int p = blockIdx.y * kTopkThreads + (int)threadIdx.x;
+  const bool in = p < P;
+  const uint32_t u = order_key(S[(size_t)bj * P + min(p, P - 1)]);   // in flight meanwhile
+  hist_bin(hist, bj, k, sh);
+  const uint32_t bin = sh.sel_bin;
+  const TopkWs f = topk_ws(tws, bj, P);
+  if (blockIdx.y == 0 && threadIdx.x == 0) {
+    f.ncand[1] = bin;
+    f.ncand[2] = (uint32_t)sh.sel_rem;
+  }
+  const uint32_t b = u >> kHistShift;
+  const uint64_t mg = __ballot(in && b > bin);
+  const uint64_t mc = __ballot(in && b == bin);
+  const int x = (blockIdx.y * kTopkThreads + w * 64) / 32;   // word of this wave's first position
+  if (lane == 0 && x * 32 < P)
+    *reinterpret_cast<uint2*>(&f.gt[x]) = make_uint2((uint32_t)mg, (uint32_t)(mg >> 32));
+  if (mc) {
+    uint32_t base = 0;
+    if (lane == 0) base = atomicAdd(f.ncand, (uint32_t)__popcll(mc));
+    base = __shfl(base, 0, 64);
+    const uint32_t r = __builtin_amdgcn_mbcnt_hi((uint32_t)(mc >> 32),
+                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)mc, 0u));
+    if (in && b == bin && base + r < (uint32_t)P) f.cand[base + r] = make_uint2(u, (uint32_t)p);
+  }
+}
+
+// Radix pass over the candidates whose bits above `shift + kDigitBits`
+// equal `prefix`: histogram of the next 10-bit digit, then the digit holding
+// the need-th largest of them.
+__device__ __forceinline__ void cand_digit_pass(const uint2* cand, int nc, uint32_t prefix,
+                                                int shift, int need, TopkShared& sh) {
+  sh.dig[threadIdx.x] = 0u;
+  __syncthreads();
+  const int top = shift + kDigitBits;
+  for (int c = threadIdx.x; c < nc; c += kTopkThreads) {
+    const uint32_t key = cand[c].x;
+    if ((key >> top) == prefix) atomicAdd(&sh.dig[(key >> shift) & (kDigitBins - 1)], 1u);
+  }
+  __syncthreads();
+  const uint32_t c1[1] = {sh.dig[threadIdx.x]};
+  __syncthreads();
+  find_bin<1>(c1, need, sh);
+}
+
+// Final top-k, one workgroup per (b, j):
+//  1. the bin of the k-th largest key (from the classification) and the
+//     candidates into LDS: the first kCandLds list entries are loaded
+//     together with the count (more candidates, in crowded or tied bins, are
+//     read from the workspace instead);
+//  2. two digit passes over the candidates give T and how many keys equal
+//     to T to take;
+//  3. per window of kMapWords bitmap words: candidates above T and equal to
+//     T are marked in two LDS bitmaps; then, one word (32 positions) per
+//     thread and round, the positions in higher bins plus the marked ones
+//     above T plus the lowest positions equal to T are written in ascending
+//     order.
+constexpr int kCandLds = 2048;
+constexpr int kMapWords = 4096;   // bitmap words per window (131072 positions)
+__global__ void __launch_bounds__(kTopkThreads)
+topk_final_kernel(uint32_t* __restrict__ tws, int32_t* __restrict__ idx, int P, int k) {
+  __shared__ TopkShared sh;
+  __shared__ uint2 lcand[kCandLds];
+  __shared__ uint32_t xgt[kMapWords], xeq[kMapWords];
+  const int bj = blockIdx.x;
+  const TopkWs f = topk_ws(tws, bj, P);
+  const uint4 hdr = *reinterpret_cast<const uint4*>(f.ncand);
+  constexpr int kPre = kCandLds / kTopkThreads;
+  uint2 pre[kPre];   // list entries loaded before the count is known (in bounds: P entries)
+#pragma unroll
+  for (int i = 0; i < kPre; ++i) pre[i] = f.cand[min((int)threadIdx.x + i * kTopkThreads, P - 1)];
+  const int nc = (int)min(hdr.x, (uint32_t)P);
+  const uint32_t bin = hdr.y;
+  const int need = (int)hdr.z;
+  const uint2* cand = f.cand;
+  if (nc <= kCandLds) {
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) lcand[threadIdx.x + i * kTopkThreads] = pre[i];
+    cand = lcand;
+    __syncthreads();
+  }
+  cand_digit_pass(cand, nc, bin, kDigitBits, need, sh);
+  const uint32_t d1 = sh.sel_bin;
+  cand_digit_pass(cand, nc, (bin << kDigitBits) | d1, 0, sh.sel_rem, sh);
+  const uint32_t T = (bin << (2 * kDigitBits)) | (d1 << kDigitBits) | sh.sel_bin;
+  const int need_eq = sh.sel_rem;   // keys equal to T to take, lowest positions first
+
+  int32_t* out = idx + (size_t)bj * k;
+  uint32_t o_base = 0, eq_base = 0;
+  const int W = (P + 31) / 32;
+  for (int m0 = 0; m0 < W; m0 += kMapWords) {
+    const int m1 = min(W, m0 + kMapWords);
+    for (int x = threadIdx.x; x < kMapWords; x += kTopkThreads) xgt[x] = xeq[x] = 0u;
+    __syncthreads();
+    for (int c = threadIdx.x; c < nc; c += kTopkThreads) {
+      const uint2 e = cand[c];
+      const int x = (int)(e.y >> 5);
+      if (x < m0 || x >= m1) continue;
+      const uint32_t bit = 1u << (e.y & 31);
+      if (e.x > T) atomicOr(&xgt[x - m0], bit);
+      else if (e.x == T) atomicOr(&xeq[x - m0], bit);
+    }
+    __syncthreads();
+    for (int x0 = m0; x0 < m1; x0 += kTopkThreads) {
+      const int x = x0 + (int)threadIdx.x;
+      const bool ok = x < m1;
+      uint32_t e = ok ? xeq[x - m0] : 0u;
+      const uint32_t g = ok ? f.gt[x] | xgt[x - m0] : 0u;
+      const int ne = __popc(e);
+      uint32_t eq_tot;
+      const int eq_before = (int)(eq_base + block_prefix_excl((uint32_t)ne, sh, eq_tot));
+      int keep = max(0, min(ne, need_eq - eq_before));
+      uint32_t kept = 0;
+      for (; keep > 0; --keep) {   // the lowest `keep` positions equal to T
+        const uint32_t low = e & (0u - e);
+        kept |= low;
+        e ^= low;
+      }
+      uint32_t sel = g | kept;
+      uint32_t sel_tot;
+      uint32_t o = o_base + block_prefix_excl((uint32_t)__popc(sel), sh, sel_tot);
+      while (sel) {
+        const int b = __builtin_ctz(sel);
+        if (o < (uint32_t)k) out[o] = x * 32 + b;   // never more than k
+        ++o;
+        sel &= sel - 1u;
+      }
+      o_base += sel_tot;
+      eq_base += eq_tot;
+    }
+    __syncthreads();   // the window's bitmaps are read before the next window clears them
   }
 }
 
 }  // namespace
 
+size_t select_topk_ws_bytes(int BH, int P) { return (size_t)BH * topk_ws_words(P) * 4; }
+
 hipError_t launch_select(const hyq_shape& s, const hyq_sizes& z, const uint16_t* Q,
                          const uint16_t* K, int32_t* idx, float* scores, float* qsum,
-                         float* cm_ws, hipStream_t st) {
+                         uint32_t* hist, uint32_t* tws, float* cm_ws, hipStream_t st) {
   if (z.k == 0) return hipSuccess;
   const int g = s.Hq / s.Hkv;
   const int t = s.window < s.L ? s.window : s.L;
   const int BH = s.B * s.Hkv;
+  // (KV head, key chunk) with the head index fastest: workgroups are spread
+  // over the XCDs round-robin, so with B*Hkv a multiple of 8 every chunk of a
+  // head (and its final top-k workgroup) runs on one XCD and shares that
+  // XCD's L2.
+  const dim3 hg(BH, (z.P + kScoreRows - 1) / kScoreRows);
   if (s.selector == HYQ_SEL_COLMASS) {
+    hist_zero_kernel<<<BH, 256, 0, st>>>(hist, tws, z.P);
     const hipError_t e = launch_colmass_scores(s, z, Q, K, scores, cm_ws, st);
     if (e != hipSuccess) return e;
+    hist_kernel<<<hg, kHistThreads, 0, st>>>(scores, hist, z.P);
   } else {
-    tail_proxy_kernel<<<BH, g * kHeadDim, g * kHeadDim * sizeof(float), st>>>(Q, qsum, s.Hq,
-                                                                                s.Hkv, s.L, t);
-    dim3 sg((z.P + 255) / 256, BH);
-    score_kernel<<<sg, 256, 0, st>>>(K, qsum, scores, s.L, z.P);
+    tail_proxy_kernel<<<s.B * s.Hq, kTailThreads, 0, st>>>(Q, qsum, hist, tws, s.Hq, s.Hkv, s.L,
+                                                           t, z.P);
+    score_kernel<<<hg, kHistThreads, 0, st>>>(K, qsum, scores, hist, g, s.L, z.P);
   }
-  topk_kernel<<<BH, kTopkThreads, 0, st>>>(scores, idx, z.P, z.k);
+  const dim3 cg(BH, (z.P + kTopkThreads - 1) / kTopkThreads);
+  topk_classify_kernel<<<cg, kTopkThreads, 0, st>>>(scores, hist, tws, z.P, z.k);
+  topk_final_kernel<<<BH, kTopkThreads, 0, st>>>(tws, idx, z.P, z.k);
   return hipGetLastError();
 }
 

@@ -16,6 +16,7 @@ SHAPES = [
     ("b2_h4_4k", 2, 8, 4, 4096, 64, 20000),
     ("ragged_b1_h8", 1, 16, 8, 3001, 77, 30000),
     ("gqa32q8kv_32k", 1, 32, 8, 32768, 256, 10000),
+    ("prefix_over_32k", 1, 8, 2, 70000, 100, 20000),   # the top-k reads its scores in 3 parts
 ]
 
 
