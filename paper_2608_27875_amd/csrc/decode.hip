@@ -42,7 +42,8 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 typedef unsigned v4u __attribute__((ext_vector_type(4)));
 typedef unsigned v2u __attribute__((ext_vector_type(2)));
 
-constexpr int kDecWaves = 4;
+constexpr int kDecWaves = kDecodeWaves;
+static_assert(kBlock == 64 && kHeadDim == 128, "decode_shape_for assumes 64-token blocks, D = 128");
 constexpr int kDecThreads = kDecWaves * 64;
 constexpr int kPartStride = kDecodePartFloats;
 constexpr float kLazyD = 8.0f;             // rescale only when the max grows by > 2^8
@@ -818,10 +819,7 @@ DecodeSplit decode_split(const hyq_dcache& c) {
   const int nbf = (c.n_frozen + kBlock - 1) / kBlock;
   d.nbq = nbf + c.n_merged;
   const int nft = (c.vl_rows + c.ring_rows) / kBlock;
-  const DecodeShape sh = choose_decode_split(
-      d.nbq, nft, (int64_t)c.B * c.Hkv, device_cus(), kDecWaves, c.bits_kv == 4 ? 4 : 2,
-      2 * kBlock * kHeadDim * c.bits_kv / 8,   // K and V codes of a block
-      2 * kBlock * kHeadDim * 2);              // K and V bf16 rows of a tile
+  const DecodeShape sh = decode_shape_for(d.nbq, nft, (int64_t)c.B * c.Hkv, device_cus(), c.bits_kv);
   d.S_q = sh.S_q;
   d.S_f = sh.S_f;
   return d;

@@ -58,4 +58,18 @@ inline DecodeShape choose_decode_split(int64_t nbq, int64_t nft, int64_t heads, 
   return d;
 }
 
+// Waves per workgroup of the decode attention kernel.
+constexpr int kDecodeWaves = 4;
+
+// The launch shape the decode kernel uses for nbq quantized blocks and nft
+// full-precision tiles per KV head at `bits` (8 or 4): the defaults above
+// filled in from the kernel's geometry (64-token blocks and tiles of 128
+// channels; u = 4 int4 or 2 8-bit blocks per wave).
+inline DecodeShape decode_shape_for(int64_t nbq, int64_t nft, int64_t heads, int64_t n_cu,
+                                    int bits) {
+  return choose_decode_split(nbq, nft, heads, n_cu, kDecodeWaves, bits == 4 ? 4 : 2,
+                             2LL * 64 * 128 * bits / 8,   // K and V codes of a block
+                             2LL * 64 * 128 * 2);         // K and V bf16 rows of a tile
+}
+
 }  // namespace hyq
