@@ -329,6 +329,26 @@ HYQ_API int hyq_decode_attn(const hyq_dcache* cache, const void* q, float softma
                             void* out, int32_t out_dtype, void* ws, size_t ws_bytes,
                             void* stream);
 
+/*
+ * hyq_decode_attn without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, runtimes
+ * that forbid hipMalloc): the same kernels and result, bit for bit, with
+ * the split partials in a scratch array of HYQ_NOALLOC_SCRATCH_BYTES that
+ * the library holds on each GPU (from its first use there until the process
+ * ends).  Nothing is allocated by this call or by the library for it.
+ * The scratch is shared by every call on a GPU: calls that overlap on one
+ * GPU (different streams, or host threads without ordering) race and give
+ * wrong results; calls ordered on one stream are fine.  The first call on
+ * a device looks up the scratch's address (once per device, with that
+ * device current), so make it outside graph capture.
+ * Errors: as hyq_decode_attn; HYQ_EUNSUPPORTED when this launch's partials
+ * (B * Hkv * splits * (Hq/Hkv) * 132 floats; about 9 MB for batch 16 at a
+ * 32k-token cache) exceed the scratch.  Nothing is enqueued on error.
+ */
+#define HYQ_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+HYQ_API int hyq_decode_attn_noalloc(const hyq_dcache* cache, const void* q, float softmax_scale,
+                                    void* out, int32_t out_dtype, void* stream);
+
 /* Static description of a return code. */
 HYQ_API const char* hyq_strerror(int code);
 

@@ -28,7 +28,7 @@ SEL_PROXY, SEL_COLMASS = 0, 1  # hyq_shape.selector
 DECODE_WS = 64                # HYQ_DECODE_WS: staging buffer capacity
 EXPORTED = ("hyq_sizes_for", "hyq_select_vertical", "hyq_quantize", "hyq_attn_prefill",
             "hyq_strerror", "hyq_last_error", "hyq_dcache_init", "hyq_freeze",
-            "hyq_decode_append", "hyq_decode_attn")
+            "hyq_decode_append", "hyq_decode_attn", "hyq_decode_attn_noalloc")
 
 
 class HyqError(RuntimeError):
@@ -119,8 +119,10 @@ def lib():
         L.hyq_decode_append.argtypes = [DC, P, P, P]
         L.hyq_decode_attn.argtypes = [DC, P, ctypes.c_float, P, ctypes.c_int32, P,
                                       ctypes.c_size_t, P]
+        L.hyq_decode_attn_noalloc.argtypes = [DC, P, ctypes.c_float, P, ctypes.c_int32, P]
         for f in ("hyq_sizes_for", "hyq_select_vertical", "hyq_quantize", "hyq_attn_prefill",
-                  "hyq_dcache_init", "hyq_freeze", "hyq_decode_append", "hyq_decode_attn"):
+                  "hyq_dcache_init", "hyq_freeze", "hyq_decode_append", "hyq_decode_attn",
+                  "hyq_decode_attn_noalloc"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -414,3 +416,20 @@ def hyq_decode_attn(cache: DecodeCache, q, out, softmax_scale: float | None = No
     _check(lib().hyq_decode_attn(ctypes.byref(cache.c), qp, ctypes.c_float(scale), o,
                                  ctypes.c_int32(out_dtype), ctypes.c_void_p(ws.data_ptr()),
                                  ctypes.c_size_t(ws.numel()), _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20   # HYQ_NOALLOC_SCRATCH_BYTES
+
+
+def hyq_decode_attn_noalloc(cache: DecodeCache, q, out, softmax_scale: float | None = None,
+                            out_dtype: int = 0, stream=None):
+    """hyq_decode_attn with the library's own per-GPU scratch instead of a
+    workspace (see include/hyq.h): allocates nothing."""
+    torch = _torch()
+    qp = _decode_rows_ok(cache, q, "q", cache.c.Hq)
+    scale = 1.0 / math.sqrt(cache.c.D) if softmax_scale is None else softmax_scale
+    odt = (torch.float32,) if out_dtype == 0 else (torch.bfloat16,)
+    nb = cache.c.B * cache.c.Hq * cache.c.D * (4 if out_dtype == 0 else 2)
+    o = _ptr(out, "out", nb, odt, cache.device)
+    _check(lib().hyq_decode_attn_noalloc(ctypes.byref(cache.c), qp, ctypes.c_float(scale), o,
+                                         ctypes.c_int32(out_dtype), _stream(stream)))

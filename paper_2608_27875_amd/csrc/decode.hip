@@ -26,6 +26,8 @@
 // partial (m, l, acc) per query head; a second kernel reduces the partials.
 #include "codes_dev.h"
 #include "decode_split.h"
+
+#include <mutex>
 #include "hyq_internal.h"
 #include "quant_dev.h"
 
@@ -799,6 +801,35 @@ decode_combine_kernel(const float* __restrict__ part, void* __restrict__ out, in
 // ---- host launchers -------------------------------------------------------
 
 // Compute units of the current device (cached per device).
+// Scratch of hyq_decode_attn_noalloc: the split partials of one launch, in
+// a file-scope device array (each GPU holds its own copy at its own address,
+// from the first use of the library on it until the process ends).  Host
+// code must not pass the array's name to a kernel: its device address comes
+// from hipGetSymbolAddress, looked up once per device with that device
+// current.
+constexpr size_t kNoAllocFloats = HYQ_NOALLOC_SCRATCH_BYTES / sizeof(float);
+__device__ __align__(256) float scratch[kNoAllocFloats];
+
+hipError_t noalloc_scratch(float** out) {
+  constexpr int kMaxDev = 64;
+  static std::mutex mu;
+  static float* addr[kMaxDev];
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDev) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = static_cast<float*>(p);
+  }
+  *out = addr[dev];
+  return hipSuccess;
+}
+
 static int device_cus() {
   constexpr int kMaxDev = 64;
   static std::atomic<int> cus[kMaxDev];
@@ -823,6 +854,12 @@ DecodeSplit decode_split(const hyq_dcache& c) {
   d.S_q = sh.S_q;
   d.S_f = sh.S_f;
   return d;
+}
+
+size_t decode_part_bytes(const hyq_dcache& c) {
+  const DecodeSplit d = decode_split(c);
+  return (size_t)c.B * c.Hkv * (size_t)(d.S_q + d.S_f) * (c.Hq / c.Hkv) * kPartStride *
+         sizeof(float);
 }
 
 size_t decode_ws_bytes(const hyq_dcache& c) {

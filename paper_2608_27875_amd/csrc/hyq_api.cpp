@@ -221,6 +221,19 @@ int check_dcache(const hyq_dcache* c) {
   return HYQ_OK;
 }
 
+// Arguments shared by the two decode attention calls.
+int check_decode_attn(const hyq_dcache* cache, const void* q, float softmax_scale, void* out,
+                      int32_t out_dtype) {
+  const int rc = check_dcache(cache);
+  if (rc) return rc;
+  if (!q || !out) return fail(HYQ_EINVAL, "q and out must be non-NULL");
+  if (out_dtype != 0 && out_dtype != 1)
+    return fail(HYQ_EINVAL, "out_dtype must be 0 (float32) or 1 (bf16), got %d", out_dtype);
+  if (!(softmax_scale > 0.0f) || softmax_scale == INFINITY)
+    return fail(HYQ_EINVAL, "softmax_scale must be positive and finite");
+  return HYQ_OK;
+}
+
 int hip_status(hipError_t e, const char* what) {
   if (e != hipSuccess) return fail(HYQ_EHIP, "%s: %s", what, hipGetErrorString(e));
   return ok();
@@ -409,21 +422,14 @@ HYQ_API int hyq_decode_append(hyq_dcache* cache, const void* k_new, const void* 
 HYQ_API int hyq_decode_attn(const hyq_dcache* cache, const void* q, float softmax_scale,
                             void* out, int32_t out_dtype, void* ws, size_t ws_bytes,
                             void* stream) {
-  const int rc = check_dcache(cache);
+  int rc = check_decode_attn(cache, q, softmax_scale, out, out_dtype);
   if (rc) return rc;
-  if (!q || !out) return fail(HYQ_EINVAL, "q and out must be non-NULL");
-  if (out_dtype != 0 && out_dtype != 1)
-    return fail(HYQ_EINVAL, "out_dtype must be 0 (float32) or 1 (bf16), got %d", out_dtype);
-  if (!(softmax_scale > 0.0f) || softmax_scale == INFINITY)
-    return fail(HYQ_EINVAL, "softmax_scale must be positive and finite");
   const size_t need = hyq::decode_ws_bytes(*cache);
   if (!ws || ws_bytes < need)
     return fail(HYQ_EINVAL, "workspace too small: %zu bytes given, %zu needed", ws_bytes, need);
   // the partials this launch writes (never more than `need`; checked so that
   // a launch can never write past the workspace)
-  const hyq::DecodeSplit d = hyq::decode_split(*cache);
-  const size_t used = (size_t)cache->B * cache->Hkv * (size_t)(d.S_q + d.S_f) *
-                      (cache->Hq / cache->Hkv) * hyq::kDecodePartFloats * sizeof(float);
+  const size_t used = hyq::decode_part_bytes(*cache);
   if (used > ws_bytes)
     return fail(HYQ_EINVAL, "workspace too small for this launch: %zu bytes given, %zu used",
                 ws_bytes, used);
@@ -431,6 +437,24 @@ HYQ_API int hyq_decode_attn(const hyq_dcache* cache, const void* q, float softma
                                             out, out_dtype, static_cast<float*>(ws),
                                             static_cast<hipStream_t>(stream)),
                     "hyq_decode_attn launch");
+}
+
+HYQ_API int hyq_decode_attn_noalloc(const hyq_dcache* cache, const void* q, float softmax_scale,
+                                    void* out, int32_t out_dtype, void* stream) {
+  int rc = check_decode_attn(cache, q, softmax_scale, out, out_dtype);
+  if (rc) return rc;
+  const size_t used = hyq::decode_part_bytes(*cache);
+  if (used > HYQ_NOALLOC_SCRATCH_BYTES)
+    return fail(HYQ_EUNSUPPORTED,
+                "this decode launch needs %zu bytes of scratch, more than the %zu bytes the "
+                "allocation-free call holds; use hyq_decode_attn with a workspace",
+                used, (size_t)HYQ_NOALLOC_SCRATCH_BYTES);
+  float* part = nullptr;
+  const hipError_t e = hyq::noalloc_scratch(&part);
+  if (e != hipSuccess) return hip_status(e, "hyq_decode_attn_noalloc scratch lookup");
+  return hip_status(hyq::launch_decode_attn(*cache, static_cast<const uint16_t*>(q), softmax_scale,
+                                            out, out_dtype, part, static_cast<hipStream_t>(stream)),
+                    "hyq_decode_attn_noalloc launch");
 }
 
 }  // extern "C"

@@ -60,6 +60,11 @@ struct DecodeSplit {
 constexpr int kDecodePartFloats = 132;   // one partial: acc[128], m, l, padding
 DecodeSplit decode_split(const hyq_dcache& c);
 size_t decode_ws_bytes(const hyq_dcache& c);
+// Partials (bytes) that one decode attention launch writes for the cache's
+// current state.
+size_t decode_part_bytes(const hyq_dcache& c);
+// Device address of the allocation-free call's scratch on the current device.
+hipError_t noalloc_scratch(float** out);
 hipError_t launch_freeze_gather(const hyq_dcache& c, int N, const uint16_t* K, const uint16_t* V,
                                 hipStream_t st);
 hipError_t launch_decode_append(const hyq_dcache& c, const uint16_t* k_new, const uint16_t* v_new,

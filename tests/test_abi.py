@@ -245,3 +245,26 @@ def test_decode_calls_reject_bad_arguments_before_launch(lib):
     assert "match" in hyq.hyq_last_error()
     assert lib.hyq_freeze(ctypes.byref(s.c()), f, f, f, ctypes.byref(c), f,
                           z["freeze_ws_bytes"] - 1, N) == hyq.HYQ_EINVAL
+
+
+def test_decode_attn_noalloc_rejects_before_launch(lib):
+    """The allocation-free decode call validates like hyq_decode_attn and
+    refuses a launch whose partials exceed its scratch, before any HIP call."""
+    fake = 0x1000
+    f = ctypes.c_void_p(fake)
+    N = None
+    s = _dshape(L=1000, window=64, budget_ppm=20000, bits_kv=8)
+    c, _ = hyq.hyq_dcache_init(s, 1200)
+    for n in hyq._DCACHE_PTRS:
+        setattr(c, n, fake)
+    assert lib.hyq_decode_attn_noalloc(ctypes.byref(c), f, ctypes.c_float(0.088), f, 2,
+                                       N) == hyq.HYQ_EINVAL
+    assert lib.hyq_decode_attn_noalloc(ctypes.byref(c), N, ctypes.c_float(0.088), f, 0,
+                                       N) == hyq.HYQ_EINVAL
+    big = _dshape(B=64, Hq=32, Hkv=8, L=32768, window=128, budget_ppm=50000, bits_kv=4)
+    cb, _ = hyq.hyq_dcache_init(big, 32768 + 64)
+    for n in hyq._DCACHE_PTRS:
+        setattr(cb, n, fake)
+    assert lib.hyq_decode_attn_noalloc(ctypes.byref(cb), f, ctypes.c_float(0.088), f, 0,
+                                       N) == hyq.HYQ_EUNSUPPORTED
+    assert "scratch" in hyq.hyq_last_error()
