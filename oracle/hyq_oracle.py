@@ -45,6 +45,13 @@ path follows the same ones):
   c_B = 6, the code the E2M1 value nearest to fl32(x / s), ties to the even
   code, saturating at +-6, the sign kept when the result is zero; Q stays at
   8 bits in E4M3 (as with 4-bit integers, whose Q is int8); codes 0..15;
+* FP4 with FP6 queries ("fp4q6"): K_Q and V_Q as for FP4; Q in OCP FP6
+  E2M3 (no infinities or NaN, largest finite 7.5) with c_B = 7.5, the code
+  the E2M3 value nearest to fl32(x / s), ties to the even code, saturating
+  at +-7.5, the sign kept when the result is zero, one code per byte
+  (bit 5 sign, bits 4..3 exponent, bits 2..0 mantissa), with the same
+  per-64-row block scale as every other Q format; so that both operands of
+  the quantized Q.K product are at most 6 bits wide;
 * causality holds by original key position in every segment;
 * bits = 16 disables quantization: every key takes the full-precision path.
 
@@ -68,7 +75,8 @@ C_INT8 = 127
 C_INT4 = 7
 C_FP8 = 448          # c_B for FP8 (Algorithm 2, Stage 2)
 C_FP4 = 6            # c_B for FP4 E2M1: its largest finite value
-FORMATS = ("int", "fp8", "fp4")
+C_FP6 = 7.5          # c_B for FP6 E2M3 queries: its largest finite value
+FORMATS = ("int", "fp8", "fp4", "fp4q6")
 
 
 # ---------------------------------------------------------------------------
@@ -169,11 +177,51 @@ def e2m1_encode(y: np.ndarray) -> np.ndarray:
     return np.where(np.signbit(y), code | np.uint8(0x8), code).astype(np.uint8)
 
 
+def e2m3_values() -> np.ndarray:
+    """Values of the 64 FP6 E2M3 codes (the OCP microscaling element format):
+    bit 5 sign, bits 4..3 exponent with bias 1, bits 2..0 mantissa; exponent
+    0 is subnormal (m/8); no infinities, no NaN; largest finite value 7.5."""
+    out = np.empty(64, dtype=np.float64)
+    for code in range(64):
+        sign = -1.0 if code & 0x20 else 1.0
+        e = (code >> 3) & 0x3
+        m = code & 0x7
+        out[code] = sign * (m / 8.0 if e == 0 else (1.0 + m / 8.0) * 2.0 ** (e - 1))
+    return out
+
+
+_E2M3 = e2m3_values()
+
+
+def e2m3_decode(codes: np.ndarray) -> np.ndarray:
+    """FP6 E2M3 codes (0..63) -> float64 values (exact)."""
+    return _E2M3[np.asarray(codes).astype(np.uint8) & 0x3F]
+
+
+def e2m3_encode(y: np.ndarray) -> np.ndarray:
+    """float32 -> FP6 E2M3 codes (uint8, 0..63): the nearest of the 32
+    magnitudes 0 .. 7.5, ties to the even code, |y| beyond 7.5 saturating to
+    7.5, the sign bit kept when the result is zero."""
+    y = np.asarray(y, dtype=np.float32)
+    mags = _E2M3[:32]                          # codes 0..31, ascending
+    a = np.minimum(np.abs(y).astype(np.float64), C_FP6)
+    hi = np.clip(np.searchsorted(mags, a, side="left"), 1, 31)
+    lo = hi - 1
+    dlo = a - mags[lo]
+    dhi = mags[hi] - a
+    code = np.where(dlo < dhi, lo, np.where(dhi < dlo, hi, np.where(lo % 2 == 0, lo, hi)))
+    code = code.astype(np.uint8)
+    return np.where(np.signbit(y), code | np.uint8(0x20), code).astype(np.uint8)
+
+
 def q_code_values(codes: np.ndarray, fmt: str) -> np.ndarray:
-    """The numbers the stored Q codes stand for (float64): E4M3 for both
-    floating-point formats (FP4 keeps the query at 8 bits), else integers."""
+    """The numbers the stored Q codes stand for (float64): E4M3 for FP8 and
+    FP4 (which keeps the query at 8 bits), E2M3 for FP4 with FP6 queries,
+    else integers."""
     if fmt in ("fp8", "fp4"):
         return e4m3_decode(codes)
+    if fmt == "fp4q6":
+        return e2m3_decode(codes)
     return np.asarray(codes).astype(np.float64)
 
 
@@ -181,7 +229,7 @@ def kv_code_values(codes: np.ndarray, fmt: str) -> np.ndarray:
     """The numbers the stored K/V codes stand for (float64)."""
     if fmt == "fp8":
         return e4m3_decode(codes)
-    if fmt == "fp4":
+    if fmt in ("fp4", "fp4q6"):
         return e2m1_decode(codes)
     return np.asarray(codes).astype(np.float64)
 
@@ -397,6 +445,24 @@ def quantize_rows_fp4(x: np.ndarray, block: int):
     return codes.reshape(nb * block, D)[:n], scales
 
 
+def quantize_rows_fp6(x: np.ndarray, block: int):
+    """Per-block FP6 quantization of rows x [n, D] (float32): Algorithm 2
+    Stage 2 with B = FP6 E2M3, c_B = 7.5, s = fl32(max|x| / 7.5), code =
+    E2M3(fl32(x / s)); s = 0 gives codes 0.  Returns (codes uint8 [n, D] in
+    0..63, scales float32)."""
+    n, D = x.shape
+    nb = -(-n // block)
+    padded = np.zeros((nb * block, D), dtype=np.float32)
+    padded[:n] = x
+    blocks = padded.reshape(nb, block, D)
+    amax = np.abs(blocks).max(axis=(1, 2))
+    scales = (amax / np.float32(C_FP6)).astype(np.float32)
+    safe = np.where(scales == 0, np.float32(1.0), scales)
+    codes = e2m3_encode((blocks / safe[:, None, None]).astype(np.float32))
+    codes[scales == 0] = 0
+    return codes.reshape(nb * block, D)[:n], scales
+
+
 def quantize(Qb, Kb, Vb, idx, W: int, bits: int, block: int = 64, fmt: str = "int"):
     """Algorithm 2, Stages 1-2 on bf16 inputs.
 
@@ -404,11 +470,14 @@ def quantize(Qb, Kb, Vb, idx, W: int, bits: int, block: int = 64, fmt: str = "in
     [B,Hq,n_qblk]; k_codes / v_codes [B,Hkv,nQ,D] (not packed), k_scale /
     v_scale [B,Hkv,n_kvblk].  ``fmt`` "int": int8 codes in [-c, c]; "fp8"
     (bits must be 8): E4M3 bit patterns (uint8) for Q, K and V; "fp4" (bits
-    must be 4): E2M1 codes (uint8, 0..15) for K and V, E4M3 for Q.  bits = 16
-    returns only kq_pos (nothing is quantized).
+    must be 4): E2M1 codes (uint8, 0..15) for K and V, E4M3 for Q; "fp4q6"
+    (bits must be 4): E2M1 for K and V, E2M3 codes (uint8, 0..63) for Q.
+    bits = 16 returns only kq_pos (nothing is quantized).
     """
-    if fmt not in FORMATS or (fmt == "fp8" and bits != 8) or (fmt == "fp4" and bits != 4):
-        raise ValueError("fmt must be 'int', 'fp8' with bits = 8, or 'fp4' with bits = 4")
+    if fmt not in FORMATS or (fmt == "fp8" and bits != 8) or \
+            (fmt in ("fp4", "fp4q6") and bits != 4):
+        raise ValueError("fmt must be 'int', 'fp8' with bits = 8, or 'fp4' / 'fp4q6' with "
+                         "bits = 4")
     B, Hq, L, D = Qb.shape
     Hkv = Kb.shape[1]
     P = max(0, L - W)
@@ -424,12 +493,12 @@ def quantize(Qb, Kb, Vb, idx, W: int, bits: int, block: int = 64, fmt: str = "in
             return quantize_rows_fp8(x, block)
         q_rows = qrows
         ctype = np.uint8
-    elif fmt == "fp4":
+    elif fmt in ("fp4", "fp4q6"):
         def qrows(x, c):
             return quantize_rows_fp4(x, block)
 
         def q_rows(x, c):
-            return quantize_rows_fp8(x, block)
+            return quantize_rows_fp8(x, block) if fmt == "fp4" else quantize_rows_fp6(x, block)
         ctype = np.uint8
     else:
         def qrows(x, c):
@@ -683,6 +752,9 @@ def freeze(Qb, Kb, Vb, Hkv: int, W: int, budget_ppm: int, bits: int, block: int 
     a multiple of the block)."""
     if bits == 16:
         raise ValueError("freeze needs a quantized format (bits 8 or 4)")
+    if fmt == "fp4q6":
+        raise ValueError("decode keeps its queries in bf16: use fmt 'fp4' (the query "
+                         "format of 'fp4q6' applies to the prefill only)")
     B, Hq, N, D = Qb.shape
     if staging < block or staging % block:
         raise ValueError("the staging capacity is a positive multiple of the block")

@@ -153,6 +153,49 @@ def quant_block_fp4_exact(vals):
     return codes, float(s)
 
 
+def e2m3_value_exact(code: int) -> Fraction:
+    """OCP FP6 E2M3 code -> exact rational, from its fields: sign bit 5,
+    exponent bits 4..3 with bias 1, mantissa bits 2..0; exponent 0 is
+    subnormal.  Written from the format definition, independently of the
+    oracle."""
+    code = int(code) & 0x3F
+    sign = -1 if code >> 5 else 1
+    e = (code >> 3) & 0x3
+    m = code & 0x7
+    if e == 0:
+        return sign * Fraction(m, 8)
+    return sign * (1 + Fraction(m, 8)) * Fraction(2) ** (e - 1)
+
+
+def e2m3_nearest(x: Fraction, negative: bool) -> int:
+    """Nearest E2M3 code to the exact value x by enumeration of all 32
+    magnitudes (ties to the even code; beyond +-7.5 the nearest is +-7.5);
+    sign bit from ``negative``."""
+    a = abs(x)
+    best, bd = None, None
+    for code in range(32):
+        d = abs(e2m3_value_exact(code) - a)
+        if bd is None or d < bd or (d == bd and code % 2 == 0 and best % 2 == 1):
+            best, bd = code, d
+    return best | (0x20 if negative else 0)
+
+
+def quant_block_fp6_exact(vals):
+    """FP6 block quantization with exact rationals: s = fl32(amax/7.5), code =
+    nearest E2M3 to fl32(x/s)."""
+    fr = [Fraction(float(v)) for v in vals]
+    amax = max(abs(v) for v in fr)
+    s = round_to_f32(amax / Fraction(15, 2))
+    if s == 0:
+        return [0] * len(fr), 0.0
+    codes = []
+    for v, raw in zip(fr, vals):
+        y = round_to_f32(v / s)
+        negative = y < 0 or (y == 0 and math.copysign(1.0, float(raw)) < 0)
+        codes.append(e2m3_nearest(y, negative))
+    return codes, float(s)
+
+
 def topk_by_rank(S, k: int):
     """Position p is chosen iff fewer than k positions beat it, where p' beats p
     when S[p'] > S[p], or S[p'] == S[p] and p' < p.  Ascending output."""
@@ -167,12 +210,13 @@ def topk_by_rank(S, k: int):
 
 def attention_rows(Qv, Kv, Vv, L, W, bits, block, idx_list, qcodes, qscales,
                    kcodes, kscales, vcodes, vscales, fp8: bool = False, band: bool = False,
-                   fp4: bool = False):
+                   fp4: bool = False, q6: bool = False):
     """Scalar-loop hybrid attention for one (batch, head).
 
     band: the per-query window (row t sees keys t+1-W .. t in full precision,
     a quantizable key only quantized when it is older than that).
-    fp8: every code is E4M3; fp4: Q codes E4M3, K/V codes E2M1.
+    fp8: every code is E4M3; fp4: Q codes E4M3, K/V codes E2M1; q6 (with
+    fp4): Q codes E2M3.
 
     Qv, Kv, Vv: lists of float rows (original positions).  idx_list: the
     vertical positions of this KV head.  q/k/v codes and scales are per
@@ -185,6 +229,8 @@ def attention_rows(Qv, Kv, Vv, L, W, bits, block, idx_list, qcodes, qscales,
     vl = set(idx_list)
 
     def cq(code):
+        if q6:
+            return float(e2m3_value_exact(code))
         return float(e4m3_value_exact(code)) if (fp8 or fp4) else int(code)
 
     def cv(code):
