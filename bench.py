@@ -39,6 +39,7 @@ if ROOT not in sys.path:
 
 INT8_PEAK_TOPS = 5000.0        # MI355X dense int8 MFMA, TOP/s
 F16_PEAK_TFLOPS = 2500.0       # MI355X dense f16/bf16 MFMA, TFLOP/s
+FP4_PEAK_TFLOPS = 10100.0      # MI355X dense fp4/fp6 MFMA, TFLOP/s
 BLENDED_PEAK = 1.0 / (0.5 / INT8_PEAK_TOPS + 0.5 / F16_PEAK_TFLOPS)   # int8 QK^T + f16 PV
 HBM_PEAK_GBS = 8000.0
 
@@ -303,9 +304,10 @@ def main():
                          "is one GPU's share of the 32k workload under 8-way head sharding")
     ap.add_argument("--no-bits16", action="store_true",
                     help="skip the full-precision (bits 16) attention of the same inputs")
-    ap.add_argument("--fmt", choices=("int", "fp8", "fp4"), default="int",
+    ap.add_argument("--fmt", choices=("int", "fp8", "fp4", "fp4q6"), default="int",
                     help="code format of the quantized path (fp8 = OCP E4M3, 8-bit only; "
-                         "fp4 = OCP E2M1 K/V with E4M3 queries, sets bits 4)")
+                         "fp4 = OCP E2M1 K/V with E4M3 queries, fp4q6 the same with FP6 E2M3 "
+                         "queries; both set bits 4)")
     ap.add_argument("--no-fp8", action="store_true",
                     help="skip the FP8-code run of the same inputs")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode measurement")
@@ -364,8 +366,9 @@ def main():
         cfg["Hq"], cfg["Hkv"] = args.hq, hkv
     Q, K, V = t(np.ascontiguousarray(d["Q"])), t(np.ascontiguousarray(d["K"])), \
         t(np.ascontiguousarray(d["V"]))
-    fmt = {"fp8": hyq.FMT_FP8, "fp4": hyq.FMT_FP4}.get(args.fmt, hyq.FMT_INT)
-    if fmt == hyq.FMT_FP4:
+    fmt = {"fp8": hyq.FMT_FP8, "fp4": hyq.FMT_FP4, "fp4q6": hyq.FMT_FP4Q6}.get(args.fmt,
+                                                                              hyq.FMT_INT)
+    if fmt in (hyq.FMT_FP4, hyq.FMT_FP4Q6):
         cfg["bits"] = 4
     cfg["fmt_name"] = args.fmt
     shape = hyq.Shape(B=cfg["B"], Hq=cfg["Hq"], Hkv=cfg["Hkv"], L=cfg["L"], window=cfg["W"],
@@ -488,11 +491,16 @@ def main():
         print("[bench] 4-bit codes (int4, fp4)", file=sys.stderr, flush=True)
         fl = causal_flops(shape.B, shape.Hq, shape.L, shape.D)
         four_bit = {}
-        for name, fx in (("int4", hyq.FMT_INT), ("fp4", hyq.FMT_FP4)):
+        for name, fx in (("int4", hyq.FMT_INT), ("fp4", hyq.FMT_FP4), ("fp4q6", hyq.FMT_FP4Q6)):
             msx = quant_attn_ms(dataclasses.replace(shape, bits_kv=4, kv_format=fx))
             tfx = fl / (msx * 1e-3) / 1e12
             four_bit[name] = {"attention_ms_median": round(msx, 4), "tflops": round(tfx, 2),
                               "frac_int8_fp8_peak": round(tfx / INT8_PEAK_TOPS, 4)}
+            if fx == hyq.FMT_FP4Q6:
+                # E2M1 keys x E2M3 queries: the Q.K MFMA runs at the 4/6-bit rate
+                four_bit[name]["frac_fp4_fp6_peak"] = round(tfx / FP4_PEAK_TFLOPS, 4)
+                four_bit[name]["note"] = ("Q.K on the 4/6-bit MFMA rate; P.V stays f16 (2.5 PF), "
+                                          "so the whole kernel cannot approach the 4-bit peak")
 
     # the same inputs with FP8 (E4M3) codes: quantize + attention
     fp8 = None
@@ -557,7 +565,7 @@ def main():
                    z["q_scale_bytes"] + 2 * z["kv_scale_bytes"] + z["kq_pos_bytes"] + z["idx_bytes"])
     workload = (f"gqa{shape.Hq}q{shape.Hkv}kv_d{shape.D}_B{shape.B}_L{shape.L}_W{shape.window}"
                 f"_r{shape.budget_ppm}ppm_kv{shape.bits_kv}bit" +
-                {hyq.FMT_FP8: "_fp8", hyq.FMT_FP4: "_fp4"}.get(fmt, ""))
+                {hyq.FMT_FP8: "_fp8", hyq.FMT_FP4: "_fp4", hyq.FMT_FP4Q6: "_fp4q6"}.get(fmt, ""))
     traffic = load_traffic(workload)
     planted = d["planted"]
     idx = bufs["idx"].cpu().numpy()
@@ -580,7 +588,8 @@ def main():
         "vs_baseline": None,
         "dtype": ("bf16" if shape.bits_kv == 16 else
                   "e4m3+f16" if fmt == hyq.FMT_FP8 else
-                  "e2m1xe4m3+f16" if fmt == hyq.FMT_FP4 else "i8+f16"),
+                  "e2m1xe4m3+f16" if fmt == hyq.FMT_FP4 else
+                  "e2m1xe2m3+f16" if fmt == hyq.FMT_FP4Q6 else "i8+f16"),
         "data": "synthetic (seeded Gaussian Q/K/V, planted vertical lines, x10 outlier K channels)",
         "config": {"workload": workload, "B": shape.B, "Hq": shape.Hq, "Hkv": shape.Hkv,
                    "L": shape.L, "D": shape.D, "window": shape.window,

@@ -69,6 +69,15 @@ extern "C" {
                            per byte like int4 (element 2i in the low nibble).  Q
                            keeps 8 bits as E4M3 codes exactly as with
                            HYQ_FMT_FP8.                                          */
+#define HYQ_FMT_FP4Q6 3 /* K and V exactly as HYQ_FMT_FP4 (bits_kv = 4); Q as OCP
+                           FP6 E2M3 codes (c = 7.5), one per byte (bit 5 sign,
+                           bits 4..3 exponent, bits 2..0 mantissa): the E2M3
+                           value nearest to x / s, ties to the even code,
+                           saturating at +-7.5, zero keeps the sign of x,
+                           s = max|x| / 7.5 per 64-row block.  Both operands of
+                           the quantized Q.K product are then at most 6 bits
+                           wide.  Prefill calls only (decode queries stay bf16;
+                           the decode cache rejects this format).             */
 
 /* Readings of the full-precision window (eq. win_def of Section 4.1). */
 #define HYQ_WIN_FIXED 0   /* the last W keys [L-W, L), as Algorithms 1, 2 and 4 use it */
@@ -91,8 +100,8 @@ typedef struct hyq_shape {
   int32_t bits_kv;           /* 16 (no quantization), 8 (int8 / E4M3) or 4 (packed
                                 int4 / E2M1), see kv_format                          */
   int32_t block;             /* quantization block in tokens (64)                   */
-  int32_t kv_format;         /* HYQ_FMT_INT, HYQ_FMT_FP8 (bits 8) or HYQ_FMT_FP4 (bits
-                                4); ignored when bits = 16                          */
+  int32_t kv_format;         /* HYQ_FMT_INT, HYQ_FMT_FP8 (bits 8), HYQ_FMT_FP4 or
+                                HYQ_FMT_FP4Q6 (bits 4); ignored when bits = 16      */
   int32_t window_mode;       /* HYQ_WIN_FIXED or HYQ_WIN_BAND                       */
   int32_t selector;          /* HYQ_SEL_PROXY or HYQ_SEL_COLMASS                    */
   int32_t staging;           /* decode only: staging capacity W_s in tokens, 0 for

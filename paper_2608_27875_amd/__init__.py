@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(_HERE, "libhyq.so")
 
 HYQ_OK, HYQ_EINVAL, HYQ_EUNSUPPORTED, HYQ_EHIP = 0, -1, -2, -3
 KQ_POS_PAD = 0x7FFFFFFF
-FMT_INT, FMT_FP8, FMT_FP4 = 0, 1, 2   # hyq_shape.kv_format
+FMT_INT, FMT_FP8, FMT_FP4, FMT_FP4Q6 = 0, 1, 2, 3   # hyq_shape.kv_format
 WIN_FIXED, WIN_BAND = 0, 1    # hyq_shape.window_mode
 SEL_PROXY, SEL_COLMASS = 0, 1  # hyq_shape.selector
 DECODE_WS = 64                # HYQ_DECODE_WS: staging buffer capacity
@@ -81,7 +81,7 @@ class Shape:
     budget_ppm: int = 0
     bits_kv: int = 8
     block: int = 64
-    kv_format: int = 0      # FMT_INT, FMT_FP8 (bits 8) or FMT_FP4 (bits 4)
+    kv_format: int = 0      # FMT_INT, FMT_FP8 (bits 8), FMT_FP4 or FMT_FP4Q6 (bits 4)
     window_mode: int = 0    # WIN_FIXED or WIN_BAND
     selector: int = 0       # SEL_PROXY (Algorithm 1) or SEL_COLMASS (eq. vl_score)
     staging: int = 0        # decode staging capacity W_s: 0 = DECODE_WS, else a multiple of 64

@@ -78,6 +78,10 @@ constexpr float kFastMax = 32768.0f;      // fast path: largest accepted weight 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kMinusBig = -1.0e30f;
 
+// Key/value codes of the two FP4 formats are the same E2M1 nibbles; they
+// differ only in the query codes (E4M3, or E2M3 for HYQ_FMT_FP4Q6).
+constexpr bool kv_fp4(int fmt) { return fmt == HYQ_FMT_FP4 || fmt == HYQ_FMT_FP4Q6; }
+
 // LDS row pitches (bytes).  +16 keeps the 16-byte reads of 8 consecutive
 // rows on distinct banks.
 // int8 K tile: 64 rows of 128 B with no padding; the 16-byte chunk j of row r
@@ -201,6 +205,11 @@ struct StageRegs {
 // products 32h .. +32; channels are assigned so that the K fragment is the
 // 16 contiguous bytes of channels 64*step + 32h .. +32, and the Q fragment
 // the two 16-byte runs at channels 64*step + 16h and 64*step + 32 + 16h.
+// E2M1 keys against E2M3 queries (HYQ_FMT_FP4Q6): the 6-bit B operand of
+// lane half h pairs element n with element n of the 4-bit A operand's half
+// h (measured with one-hot operands), its 32 codes packed 6 bits apart in
+// six registers; so the Q fragment is channels 64*step + 32h .. +32, the
+// same channels as the K fragment, packed from one code byte each.
 template <int FMT>
 struct KFrag {
   v4i f[2][4];
@@ -211,6 +220,10 @@ struct KFrag<HYQ_FMT_FP8> {
 };
 template <>
 struct KFrag<HYQ_FMT_FP4> {
+  v4i f[2][2];
+};
+template <>
+struct KFrag<HYQ_FMT_FP4Q6> {
   v4i f[2][2];
 };
 template <int FMT>
@@ -225,6 +238,10 @@ template <>
 struct QFrag<HYQ_FMT_FP4> {
   v8i f[2];
 };
+template <>
+struct QFrag<HYQ_FMT_FP4Q6> {   // six registers of packed E2M3 codes per step
+  v8i f[2];
+};
 
 template <int FMT>
 __device__ __forceinline__ void read_kfrag(KFrag<FMT>& kf, const KBuf& b, int col, int half) {
@@ -237,7 +254,7 @@ __device__ __forceinline__ void read_kfrag(KFrag<FMT>& kf, const KBuf& b, int co
         const v4i hi = *reinterpret_cast<const v4i*>(b.k + kswz(kh * 32 + col, kk * 4 + half * 2 + 1));
         kf.f[kh][kk] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       }
-    } else if constexpr (FMT == HYQ_FMT_FP4) {
+    } else if constexpr (kv_fp4(FMT)) {
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
         kf.f[kh][kk] = *reinterpret_cast<const v4i*>(b.k + kswz4(kh * 32 + col, kk * 2 + half));
@@ -261,6 +278,24 @@ __device__ __forceinline__ void read_qfrag(QFrag<FMT>& qf, const int8_t* qrow, b
       const v4i lo = ok ? *reinterpret_cast<const v4i*>(qrow + kk * 64 + half * 16) : v4i{};
       const v4i hi = ok ? *reinterpret_cast<const v4i*>(qrow + kk * 64 + 32 + half * 16) : v4i{};
       qf.f[kk] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+  } else if constexpr (FMT == HYQ_FMT_FP4Q6) {
+    // 32 code bytes (channels 64*kk + 32*half ..) -> 6-bit slots 0..31 of six
+    // registers (slot n at bits 6n .. 6n+5); done once per wave
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const v4u lo = ok ? *reinterpret_cast<const v4u*>(qrow + kk * 64 + half * 32) : v4u{};
+      const v4u hi = ok ? *reinterpret_cast<const v4u*>(qrow + kk * 64 + half * 32 + 16) : v4u{};
+      const uint32_t w[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      uint32_t r[6] = {0u, 0u, 0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int n = 0; n < 32; ++n) {
+        const uint32_t code = (w[n >> 2] >> (8 * (n & 3))) & 0x3Fu;
+        const int bit = 6 * n;
+        r[bit >> 5] |= code << (bit & 31);
+        if ((bit & 31) > 26) r[(bit >> 5) + 1] |= code >> (32 - (bit & 31));
+      }
+      qf.f[kk] = v8i{(int)r[0], (int)r[1], (int)r[2], (int)r[3], (int)r[4], (int)r[5], 0, 0};
     }
   } else {
 #pragma unroll
@@ -289,6 +324,13 @@ __device__ __forceinline__ void qk_tile(SVec<FMT> (&s)[2], const KFrag<FMT>& kf,
       for (int kk = 0; kk < 2; ++kk) {   // A format 4 = E2M1 (4 registers), B format 0 = E4M3
         const v8i ka = __builtin_shufflevector(kf.f[kh][kk], v4i{}, 0, 1, 2, 3, 4, 5, 6, 7);
         s[kh] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ka, qf.f[kk], s[kh], 4, 0, 0, 127,
+                                                                0, 127);
+      }
+    } else if constexpr (FMT == HYQ_FMT_FP4Q6) {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {   // A format 4 = E2M1, B format 2 = E2M3 (6 registers)
+        const v8i ka = __builtin_shufflevector(kf.f[kh][kk], v4i{}, 0, 1, 2, 3, 4, 5, 6, 7);
+        s[kh] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ka, qf.f[kk], s[kh], 4, 2, 0, 127,
                                                                 0, 127);
       }
     } else {
@@ -363,7 +405,7 @@ __device__ __forceinline__ void stage_store(KBuf& kb, VBuf& vb, const StageRegs<
       *reinterpret_cast<v4u*>(dst) = v4u{h[0], h[1], h[4], h[5]};
       *reinterpret_cast<v4u*>(dst + 16) = v4u{h[2], h[3], h[6], h[7]};
     }
-  } else if constexpr (FMT == HYQ_FMT_FP4) {
+  } else if constexpr (kv_fp4(FMT)) {
     // E2M1 K: the 16-byte chunk as it is (the MFMA reads 4-bit operands);
     // V: E2M1 -> f16 times 2^e, two codes per conversion, exact
     const int q4 = chunk_id<BITS>(tid, 0);
@@ -559,7 +601,7 @@ __device__ __forceinline__ void segA_tile(Smem& sm, const SegA& a, int c, const 
                                           NState& st, const v8h (&pprev)[4], v8h (&pcur)[4],
                                           StageRegs<BITS>& sr, KFrag<FMT>& kf) {
   // 4-bit integer codes are staged as 16*code
-  constexpr float kSub = (BITS == 8 || FMT == HYQ_FMT_FP4) ? 1.0f : 0.0625f;
+  constexpr float kSub = (BITS == 8 || kv_fp4(FMT)) ? 1.0f : 0.0625f;
   const int tid = threadIdx.x;
   const KBuf& cur = sm.q.kb[PH];
   const VBuf& prv = sm.q.vb[(PH + 1) & 1];
@@ -922,6 +964,9 @@ hipError_t launch_attn_prefill(const hyq_shape& s, const hyq_sizes& z, const uin
   } else if (s.bits_kv == 4 && s.kv_format == HYQ_FMT_FP4) {
     if (out_dtype) HYQ_LAUNCH(4, 1, HYQ_FMT_FP4);
     HYQ_LAUNCH(4, 0, HYQ_FMT_FP4);
+  } else if (s.bits_kv == 4 && s.kv_format == HYQ_FMT_FP4Q6) {
+    if (out_dtype) HYQ_LAUNCH(4, 1, HYQ_FMT_FP4Q6);
+    HYQ_LAUNCH(4, 0, HYQ_FMT_FP4Q6);
   } else if (s.bits_kv == 8 && s.kv_format == HYQ_FMT_FP8) {
     if (out_dtype) HYQ_LAUNCH(8, 1, HYQ_FMT_FP8);
     HYQ_LAUNCH(8, 0, HYQ_FMT_FP8);

@@ -43,12 +43,14 @@ int check_shape(const hyq_shape* s, hyq_sizes* z) {
   if (s->block < 1) return fail(HYQ_EINVAL, "block must be >= 1 (got %d)", s->block);
   if (s->bits_kv != 16 && s->bits_kv != 8 && s->bits_kv != 4)
     return fail(HYQ_EUNSUPPORTED, "bits_kv must be 16, 8 or 4 (got %d)", s->bits_kv);
-  if (s->kv_format != HYQ_FMT_INT && s->kv_format != HYQ_FMT_FP8 && s->kv_format != HYQ_FMT_FP4)
-    return fail(HYQ_EINVAL, "kv_format must be HYQ_FMT_INT, HYQ_FMT_FP8 or HYQ_FMT_FP4 (got %d)",
+  if (s->kv_format != HYQ_FMT_INT && s->kv_format != HYQ_FMT_FP8 && s->kv_format != HYQ_FMT_FP4 &&
+      s->kv_format != HYQ_FMT_FP4Q6)
+    return fail(HYQ_EINVAL,
+                "kv_format must be HYQ_FMT_INT, HYQ_FMT_FP8, HYQ_FMT_FP4 or HYQ_FMT_FP4Q6 (got %d)",
                 s->kv_format);
   if (s->kv_format == HYQ_FMT_FP8 && s->bits_kv == 4)
     return fail(HYQ_EINVAL, "FP8 codes need bits_kv = 8 (got 4)");
-  if (s->kv_format == HYQ_FMT_FP4 && s->bits_kv == 8)
+  if ((s->kv_format == HYQ_FMT_FP4 || s->kv_format == HYQ_FMT_FP4Q6) && s->bits_kv == 8)
     return fail(HYQ_EINVAL, "FP4 codes need bits_kv = 4 (got 8)");
   if (s->selector != HYQ_SEL_PROXY && s->selector != HYQ_SEL_COLMASS)
     return fail(HYQ_EINVAL, "selector must be HYQ_SEL_PROXY or HYQ_SEL_COLMASS (got %d)",
@@ -145,6 +147,9 @@ int dcache_geometry(const hyq_shape* s, int64_t max_tokens, hyq_dcache* c, hyq_d
   if (rc) return rc;
   if (s->bits_kv == 16)
     return fail(HYQ_EINVAL, "the decode cache needs a quantized format (bits_kv 8 or 4)");
+  if (s->kv_format == HYQ_FMT_FP4Q6)
+    return fail(HYQ_EINVAL, "decode keeps its queries in bf16: use HYQ_FMT_FP4 for the cache "
+                            "(HYQ_FMT_FP4Q6 sets the prefill's query codes)");
   const int32_t ws = s->staging ? s->staging : HYQ_DECODE_WS;
   if (s->window < ws)
     return fail(HYQ_EINVAL, "decode needs window >= the staging capacity %d (a merge moves that "

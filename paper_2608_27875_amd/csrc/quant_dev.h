@@ -60,10 +60,27 @@ __device__ __forceinline__ int quant1_fp4(float x, float s) {
   return c | (int)((__float_as_uint(y) >> 31) << 3);
 }
 
+// E2M3 code (0..63) of x / s (s > 0): the nearest of the 32 magnitudes
+// (eighths below 2, quarters up to 4, halves up to 7.5), a tie going to the
+// even code, beyond 7.5 the largest; bit 5 is the sign of the quotient.
+// Within each binade [0,1), [1,2), [2,4), [4,8) the magnitudes are evenly
+// spaced and start at an even code, so the nearest one is the binade's
+// first code plus rint((a - base) / step), computed exactly.
+__device__ __forceinline__ int quant1_fp6(float x, float s) {
+  const float y = x / s;
+  const float a = fabsf(y);
+  const float base = a < 1.0f ? 0.0f : a < 2.0f ? 1.0f : a < 4.0f ? 2.0f : 4.0f;
+  const float inv = a < 2.0f ? 8.0f : a < 4.0f ? 4.0f : 2.0f;
+  const int c0 = a < 1.0f ? 0 : a < 2.0f ? 8 : a < 4.0f ? 16 : 24;
+  const int c = min(31, c0 + (int)__builtin_rintf(fminf(a - base, 8.0f) * inv));
+  return c | (int)((__float_as_uint(y) >> 31) << 5);
+}
+
 template <int FMT>
 __device__ __forceinline__ int quant_code(float x, float s, float c) {
   if (FMT == HYQ_FMT_FP8) return quant1_fp8(x, s);
   if (FMT == HYQ_FMT_FP4) return quant1_fp4(x, s);
+  if (FMT == HYQ_FMT_FP4Q6) return quant1_fp6(x, s);
   return quant1(x, s, c);
 }
 

@@ -59,7 +59,7 @@ template <int FMT>
 __global__ void __launch_bounds__(kQuantThreads)
 quant_q_kernel(const uint16_t* __restrict__ Q, int8_t* __restrict__ qc, float* __restrict__ qs,
                int L, int n_qblk) {
-  constexpr float C = FMT == HYQ_FMT_FP8 ? 448.0f : 127.0f;
+  constexpr float C = FMT == HYQ_FMT_FP8 ? 448.0f : FMT == HYQ_FMT_FP4Q6 ? 7.5f : 127.0f;
   __shared__ float red[kQuantThreads / 64];
   const int bh = blockIdx.y, blk = blockIdx.x;
   const int row = threadIdx.x >> 2, c0 = (threadIdx.x & 3) * 32;
@@ -213,7 +213,7 @@ void launch_quant_kv(int bits, int fmt, const uint16_t* K, const uint16_t* V,
                      hipStream_t st) {
   if (n_blocks <= 0) return;
   dim3 kg(n_blocks, BHkv);
-  if (fmt == HYQ_FMT_FP4)
+  if (fmt == HYQ_FMT_FP4 || fmt == HYQ_FMT_FP4Q6)   // the same E2M1 key/value codes
     quant_kv_kernel<4, HYQ_FMT_FP4><<<kg, kQuantThreads, 0, st>>>(
         K, V, kq_pos, k_codes, k_scale, v_codes, v_scale, L, nQ, blk_stride);
   else if (fmt == HYQ_FMT_FP8)
@@ -235,7 +235,10 @@ hipError_t launch_quantize(const hyq_shape& s, const hyq_sizes& z, const uint16_
   const int BHkv = s.B * s.Hkv;
   launch_compact(idx, kq_pos, z.k, z.P, z.nQ, z.n_kvblk * kBlock, BHkv, st);
   dim3 qg(z.n_qblk, s.B * s.Hq);
-  if (s.kv_format != HYQ_FMT_INT)   // E4M3 queries for both floating-point formats
+  if (s.kv_format == HYQ_FMT_FP4Q6)   // E2M3 queries
+    quant_q_kernel<HYQ_FMT_FP4Q6><<<qg, kQuantThreads, 0, st>>>(Q, q_codes, q_scale, s.L,
+                                                                z.n_qblk);
+  else if (s.kv_format != HYQ_FMT_INT)   // E4M3 queries for FP8 and FP4
     quant_q_kernel<HYQ_FMT_FP8><<<qg, kQuantThreads, 0, st>>>(Q, q_codes, q_scale, s.L, z.n_qblk);
   else
     quant_q_kernel<HYQ_FMT_INT><<<qg, kQuantThreads, 0, st>>>(Q, q_codes, q_scale, s.L, z.n_qblk);

@@ -24,7 +24,8 @@ def shape_of(cfg) -> hyq.Shape:
 
 def fmt_name(shape) -> str:
     """Oracle format name of a Shape or a decode cache struct."""
-    return {hyq.FMT_FP8: "fp8", hyq.FMT_FP4: "fp4"}.get(shape.kv_format, "int")
+    return {hyq.FMT_FP8: "fp8", hyq.FMT_FP4: "fp4", hyq.FMT_FP4Q6: "fp4q6"}.get(shape.kv_format,
+                                                                               "int")
 
 
 def run_gpu(shape: hyq.Shape, d, out_dtype=0, keep_out_on_gpu=False, tensors=None):
@@ -60,7 +61,7 @@ def run_gpu(shape: hyq.Shape, d, out_dtype=0, keep_out_on_gpu=False, tensors=Non
 def unpack_codes4(raw: np.ndarray, fmt: int) -> np.ndarray:
     """Packed 4-bit codes -> one code per element: two's-complement int4
     values, or E2M1 codes 0..15 for FP4."""
-    if fmt == hyq.FMT_FP4:
+    if fmt in (hyq.FMT_FP4, hyq.FMT_FP4Q6):
         out = np.empty(raw.shape[:-1] + (raw.shape[-1] * 2,), dtype=np.uint8)
         out[..., 0::2] = raw & 0xF
         out[..., 1::2] = raw >> 4

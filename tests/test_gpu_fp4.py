@@ -1,7 +1,8 @@
-"""GPU parity for FP4 codes (OCP E2M1 keys and values with c_B = 6, E4M3
-queries): the HIP path through the C ABI against the CPU oracle on the same
-seeded inputs.  Selection, partition, code bytes and scales bit-exact;
-attention output within max-abs 2e-3 and mean-abs 2e-4."""
+"""GPU parity for FP4 codes (OCP E2M1 keys and values with c_B = 6), with
+E4M3 queries (HYQ_FMT_FP4) and with FP6 E2M3 queries (HYQ_FMT_FP4Q6, both
+MFMA operands at most 6 bits): the HIP path through the C ABI against the
+CPU oracle on the same seeded inputs.  Selection, partition, code bytes and
+scales bit-exact; attention output within max-abs 2e-3 and mean-abs 2e-4."""
 import zlib
 
 import numpy as np
@@ -14,6 +15,8 @@ from paper_2608_27875_amd import gen
 pytestmark = pytest.mark.gpu
 
 FP4 = gc.hyq.FMT_FP4
+FP4Q6 = gc.hyq.FMT_FP4Q6
+FMTS = pytest.mark.parametrize("fmt", [FP4, FP4Q6], ids=["q8", "q6"])
 
 # (name, B, Hq, Hkv, L, W, budget_ppm)
 SMALL = [
@@ -35,9 +38,9 @@ def _inputs(name, B, Hq, Hkv, L, W, seed=0):
                         W=max(W, 1), plant=0.02)
 
 
-def _shape(B, Hq, Hkv, L, W, ppm, window_mode=0):
+def _shape(B, Hq, Hkv, L, W, ppm, window_mode=0, fmt=FP4):
     return gc.hyq.Shape(B=B, Hq=Hq, Hkv=Hkv, L=L, window=W, budget_ppm=ppm, bits_kv=4,
-                        kv_format=FP4, window_mode=window_mode)
+                        kv_format=fmt, window_mode=window_mode)
 
 
 def _check_small(d, shape, skip_channel=None):
@@ -60,21 +63,24 @@ def _check_small(d, shape, skip_channel=None):
     return g
 
 
+@FMTS
 @pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
-def test_fp4_small_full_parity(case):
+def test_fp4_small_full_parity(case, fmt):
     name, B, Hq, Hkv, L, W, ppm = case
-    print(f"case {name}", flush=True)
+    print(f"case {name} fmt {fmt}", flush=True)
     d = _inputs(name, B, Hq, Hkv, L, W)
-    _check_small(d, _shape(B, Hq, Hkv, L, W, ppm))
+    _check_small(d, _shape(B, Hq, Hkv, L, W, ppm, fmt=fmt))
 
 
-def test_fp4_band_window():
+@FMTS
+def test_fp4_band_window(fmt):
     """The per-query window with FP4 codes."""
     d = _inputs("fp4_band", 1, 8, 2, 900, 96)
-    _check_small(d, _shape(1, 8, 2, 900, 96, 20000, window_mode=gc.hyq.WIN_BAND))
+    _check_small(d, _shape(1, 8, 2, 900, 96, 20000, window_mode=gc.hyq.WIN_BAND, fmt=fmt))
 
 
-def test_fp4_zeros_signs_and_saturation():
+@FMTS
+def test_fp4_zeros_signs_and_saturation(fmt):
     """Blocks with exact zeros and negative zeros (E2M1 codes 0 / 8), a block
     that is all zero (scale 0), tiny entries that round to signed zero, and
     one huge outlier (its code is +-6; in V it makes one block's scale dwarf
@@ -90,24 +96,29 @@ def test_fp4_zeros_signs_and_saturation():
         x[..., 130:140, 7] = 1e-6 * np.sign(x[..., 130:140, 7] + 0.5)
         x[..., 200, 9] = 3.0e4                         # one outlier in a block
         d[name] = gen.f32_to_bf16_bits(x)
-    g = _check_small(d, _shape(1, 4, 1, L, W, 30000), skip_channel=9)
-    nib = gc.unpack_codes4(g["k_codes"].view(np.uint8), FP4)
+    g = _check_small(d, _shape(1, 4, 1, L, W, 30000, fmt=fmt), skip_channel=9)
+    nib = gc.unpack_codes4(g["k_codes"].view(np.uint8), fmt)
     assert np.any(nib == 0x8) and np.any(nib == 0x7)
+    if fmt == FP4Q6:   # E2M3 query codes: -0 and +-7.5 occur
+        qc = g["q_codes"].view(np.uint8)
+        assert np.any(qc == 0x20) and np.any((qc & 0x1F) == 0x1F) and qc.max() <= 0x3F
 
 
-def test_fp4_deterministic():
+@FMTS
+def test_fp4_deterministic(fmt):
     d = _inputs("fp4_det", 1, 8, 2, 900, 64)
-    shape = _shape(1, 8, 2, 900, 64, 20000)
+    shape = _shape(1, 8, 2, 900, 64, 20000, fmt=fmt)
     g1 = gc.run_gpu(shape, d)
     g2 = gc.run_gpu(shape, d)
     for k in ("idx", "q_codes", "k_codes", "v_codes", "kq_pos", "out"):
         np.testing.assert_array_equal(g1[k], g2[k], err_msg=k)
 
 
+@FMTS
 @pytest.mark.timeout(300)
-def test_fp4_32k():
+def test_fp4_32k(fmt):
     """The 32k GQA workload with FP4 codes (4 heads x 512 sampled rows)."""
-    cfg = gen.workload(gen.GQA_32K, bits=4, fmt=FP4)
+    cfg = gen.workload(gen.GQA_32K, bits=4, fmt=fmt)
     print("32k fp4: generating", flush=True)
     d = gen.generate_workload(gen.GQA_32K, seed=0)
     shape = gc.shape_of(cfg)
@@ -130,11 +141,12 @@ def test_fp4_32k():
     assert mx <= gc.TOL_MAX and mean <= gc.TOL_MEAN
 
 
+@FMTS
 @pytest.mark.timeout(600)
-def test_fp4_128k():
+def test_fp4_128k(fmt):
     """The 131k-token workload (window 512, 0.5% budget) with FP4 codes:
     selection and every code in full, attention on 2 heads x 256 rows."""
-    cfg = gen.workload(gen.GQA_128K, bits=4, fmt=FP4)
+    cfg = gen.workload(gen.GQA_128K, bits=4, fmt=fmt)
     print("128k fp4: generating", flush=True)
     d = gen.generate_workload(gen.GQA_128K, seed=0)
     shape = gc.shape_of(cfg)
