@@ -13,9 +13,12 @@
 //              the f16 MFMA on the V codes (int8, E4M3 and E2M1 values are
 //              exact in f16);
 //   segments B and C: the full-precision keys (vertical lines, then the
-//              window), 64 at a time gathered into LDS: S^T with the bf16
-//              MFMA; P V with the bf16 MFMA on bf16 V, P split into a high
-//              and a low bf16 part so that P keeps ~16 bits.
+//              window), 64 at a time gathered into two alternating LDS
+//              buffers a tile ahead through registers: S^T with the bf16
+//              MFMA; P V with the f16 MFMA on V / sVref converted to f16
+//              (exact for bf16 values of that range), or, for a tile whose
+//              V / sVref leaves the f16 range, with the bf16 MFMA on raw V
+//              and P split into a high and a low bf16 part (~16 bits).
 // Causality is by original key position in every segment.  With the
 // per-query window (HYQ_WIN_BAND) row t sees keys t+1-W .. t in full
 // precision and a quantized key only once it is older than that: segment A
@@ -115,14 +118,18 @@ struct QRing {
   VBuf vb[2];
 };
 struct FBuf {                       // one full-precision tile
-  alignas(16) uint8_t k[kTile * kKPitchBf];
-  alignas(16) uint8_t v[kVBytes];
-  int32_t pos[kTile];               // rows t >= pos see the key ...
-  int32_t hi[kTile];                // ... up to row hi
+  alignas(16) uint8_t k[kTile * kKPitchBf];   // bf16 K rows
+  alignas(16) uint8_t v[kVBytes];             // V^T as f16 V / sVref
+  alignas(16) int32_t pos[kTile];             // rows t >= pos see the key ...
+  alignas(16) int32_t hi[kTile];              // ... up to row hi
+  int32_t ovf;     // (f << 8) | E: tile f staged here had a V / sVref outside the f16
+                   // range, E the largest biased float exponent of its V values
 };
+// Full-precision tiles alternate between two buffers: tile f+1 is written
+// while tile f is computed.
 union Smem {
   QRing q;
-  FBuf f;
+  FBuf f[2];
 };
 
 __device__ __forceinline__ float xhalf_max(float x) {
@@ -457,59 +464,199 @@ __device__ __forceinline__ void stage_store(KBuf& kb, VBuf& vb, const StageRegs<
   kb.pos[w == 0 ? lane : (w == 1 ? min(kMetaSK + lane, kMetaSink) : kMetaSink)] = r.meta;
 }
 
-// Stage full-precision tile: entries e0 .. e0+63 of the list
-// [vertical positions (nvl of them), then base, base+1, ...]; entries at or
-// beyond `count` are padding (position HYQ_KQ_POS_PAD, zero rows).
 // The full-precision key list of a workgroup: nvl vertical lines (idx, seen
 // from their position on), then nqb quantizable keys of the per-query band
 // (kq[nq0 ..], each seen by the W rows from its position on), then the
 // window positions base .. (seen from their position on; in band mode by W
-// rows, which is every later row).  Entries [e0, e0 + 64) are staged.
-__device__ __forceinline__ void stage_fp(FBuf& b, const uint16_t* __restrict__ Kh,
-                                         const uint16_t* __restrict__ Vh,
-                                         const int32_t* __restrict__ vl, int nvl,
-                                         const int32_t* __restrict__ kq, int nq0, int nqb,
-                                         int base, int e0, int count, int L, int band_w) {
-  const int tid = threadIdx.x;
-  if (tid < kTile) {
-    const int e = e0 + tid;
-    int p = HYQ_KQ_POS_PAD, hi = -1;
-    if (e < count) {
-      if (e < nvl) {
-        p = vl[e];
-        hi = INT32_MAX;
-      } else if (e < nvl + nqb) {
-        p = kq[nq0 + (e - nvl)];
-        hi = p + band_w - 1;
-      } else {
-        p = base + (e - nvl - nqb);
-        hi = band_w > 0 ? p + band_w - 1 : INT32_MAX;
+// rows, which is every later row).  Entries at or beyond `count` are padding
+// (position HYQ_KQ_POS_PAD, seen by no row, zero rows).
+struct FpList {
+  const int32_t* vl;
+  const int32_t* kq;
+  const int32_t* dummy;   // any readable word (entries whose position is computed)
+  int nvl, nq0, nqb, base, count, band_w;
+};
+// Entry e's position comes from a load (vertical lines, band keys) or is
+// computed (window); fp_src gives the word to load, always readable, and
+// fp_resolve turns the loaded word into (position, last row).
+__device__ __forceinline__ const int32_t* fp_src(const FpList& f, int e) {
+  return e < f.nvl ? f.vl + e : (e < f.nvl + f.nqb ? f.kq + (f.nq0 + (e - f.nvl)) : f.dummy);
+}
+__device__ __forceinline__ void fp_resolve(const FpList& f, int e, int32_t w, int& p, int& hi) {
+  if (e >= f.count) {
+    p = HYQ_KQ_POS_PAD;
+    hi = -1;
+  } else if (e < f.nvl) {
+    p = w;
+    hi = INT32_MAX;
+  } else if (e < f.nvl + f.nqb) {
+    p = w;
+    hi = w + f.band_w - 1;
+  } else {
+    p = f.base + (e - f.nvl - f.nqb);
+    hi = f.band_w > 0 ? p + f.band_w - 1 : INT32_MAX;
+  }
+}
+
+// A full-precision tile in registers.  K: thread tid holds the 16-byte
+// chunks q = tid + i * kThreads (key q / 16, channels 8 * (q % 16) ..), with
+// the key's position and last row.  V: item q = tid + i * kThreads is the
+// chunk q / 32 of the key pair (2 * (q % 32), +1), so that one LDS store
+// writes both keys of a channel (adjacent V^T slots) and the 64 lanes of a
+// wave (32 pairs, two chunks) hit distinct banks.  Also the position words of
+// the same keys of the following tile.
+constexpr int kFpPairs = kTile * 16 / kThreads;
+constexpr int kFpVItems = (kTile / 2) * 16 / kThreads;
+static_assert((kTile * 16) % kThreads == 0 && ((kTile / 2) * 16) % kThreads == 0,
+              "full-precision chunks must split evenly");
+struct FpRegs {
+  v4u k[kFpPairs], v[2 * kFpVItems];
+  int32_t pos[kFpPairs], hi[kFpPairs], vpos[2 * kFpVItems];
+  int32_t wnext[kFpPairs], vwnext[2 * kFpVItems];
+};
+__device__ __forceinline__ int fp_kkey(int i) { return ((int)threadIdx.x + i * kThreads) >> 4; }
+__device__ __forceinline__ int fp_vkey(int i, int s) {
+  return 2 * (((int)threadIdx.x + i * kThreads) & 31) + s;
+}
+__device__ __forceinline__ int fp_vchunk(int i) { return ((int)threadIdx.x + i * kThreads) >> 5; }
+
+// Position words of tile ft (before its first fp_load).
+__device__ __forceinline__ void fp_load_words(FpRegs& r, const FpList& f, int ft) {
+#pragma unroll
+  for (int i = 0; i < kFpPairs; ++i) r.wnext[i] = *fp_src(f, ft * kTile + fp_kkey(i));
+#pragma unroll
+  for (int i = 0; i < kFpVItems; ++i)
+#pragma unroll
+    for (int s = 0; s < 2; ++s) r.vwnext[2 * i + s] = *fp_src(f, ft * kTile + fp_vkey(i, s));
+}
+
+// Load the rows of tile ft (padding rows read row 0, zeroed at the store)
+// from the position words loaded earlier, then the words of tile ft+1.
+// Tiles past the end are all padding.
+__device__ __forceinline__ void fp_load(FpRegs& r, const FpList& f, const uint16_t* __restrict__ Kh,
+                                        const uint16_t* __restrict__ Vh, int ft, int L) {
+#pragma unroll
+  for (int i = 0; i < kFpPairs; ++i) {
+    int p, hi;
+    fp_resolve(f, ft * kTile + fp_kkey(i), r.wnext[i], p, hi);
+    r.pos[i] = p;
+    r.hi[i] = hi;
+    const size_t row = (unsigned)p < (unsigned)L ? (size_t)p : 0;
+    r.k[i] = reinterpret_cast<const v4u*>(Kh + row * kHeadDim)[((int)threadIdx.x + i * kThreads) & 15];
+  }
+#pragma unroll
+  for (int i = 0; i < kFpVItems; ++i)
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      int p, hi;
+      fp_resolve(f, ft * kTile + fp_vkey(i, s), r.vwnext[2 * i + s], p, hi);
+      r.vpos[2 * i + s] = p;
+      const size_t row = (unsigned)p < (unsigned)L ? (size_t)p : 0;
+      r.v[2 * i + s] = reinterpret_cast<const v4u*>(Vh + row * kHeadDim)[fp_vchunk(i)];
+    }
+  fp_load_words(r, f, ft + 1);
+}
+
+// f16 V / sVref of one bf16 value held in the high half of w (sVref a power
+// of two: exact for bf16 values of that range, down to the f16 subnormals);
+// `big` collects the largest |V| bits of values whose ratio leaves the f16
+// range.
+__device__ __forceinline__ _Float16 fp_v16(uint32_t w, float inv_vref, uint32_t& big) {
+  const float x = __uint_as_float(w) * inv_vref;
+  if (!(fabsf(x) <= 65504.0f)) big = max(big, w & 0x7fffffffu);
+  return (_Float16)x;
+}
+
+// V^T stores of one key pair (adjacent slots from the even key's) and one
+// 16-byte chunk: channel d gets the 32-bit word (f16 of key 2m, of key 2m+1).
+__device__ __forceinline__ void fp_store_vpair(FBuf& b, v4u v0, v4u v1, int key0, int chunk,
+                                               float inv_vref, uint32_t& big) {
+  const int slot = vslot(key0);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int d = chunk * 8 + 2 * j;
+    v2h lo, hi;
+    lo[0] = fp_v16(v0[j] << 16, inv_vref, big);
+    lo[1] = fp_v16(v1[j] << 16, inv_vref, big);
+    hi[0] = fp_v16(v0[j] & 0xffff0000u, inv_vref, big);
+    hi[1] = fp_v16(v1[j] & 0xffff0000u, inv_vref, big);
+    *reinterpret_cast<v2h*>(b.v + d * kVPitch + slot * 2) = lo;
+    *reinterpret_cast<v2h*>(b.v + (d + 1) * kVPitch + slot * 2) = hi;
+  }
+}
+
+// Write a loaded tile to LDS: K rows as bf16, V^T as f16 V / sVref,
+// positions and last rows.  A V ratio outside the f16 range records
+// (tile << 8) | (largest biased exponent) in ovf.
+__device__ __forceinline__ void fp_store(FBuf& b, const FpRegs& r, float inv_vref, int tag, int L) {
+#pragma unroll
+  for (int i = 0; i < kFpPairs; ++i) {
+    const int e = fp_kkey(i), col = ((int)threadIdx.x + i * kThreads) & 15;
+    const unsigned keep = (unsigned)r.pos[i] < (unsigned)L ? 0xffffffffu : 0u;
+    *reinterpret_cast<v4u*>(b.k + e * kKPitchBf + col * 16) = r.k[i] & keep;
+    if (col == 0) {
+      b.pos[e] = r.pos[i];
+      b.hi[e] = r.hi[i];
+    }
+  }
+  uint32_t big = 0;
+#pragma unroll
+  for (int i = 0; i < kFpVItems; ++i) {
+    const unsigned k0 = (unsigned)r.vpos[2 * i] < (unsigned)L ? 0xffffffffu : 0u;
+    const unsigned k1 = (unsigned)r.vpos[2 * i + 1] < (unsigned)L ? 0xffffffffu : 0u;
+    fp_store_vpair(b, r.v[2 * i] & k0, r.v[2 * i + 1] & k1, fp_vkey(i, 0), fp_vchunk(i),
+                   inv_vref, big);
+  }
+  if (big != 0) atomicMax(&b.ovf, (tag << 8) | (int)(big >> 23));
+}
+
+// Rewrite the V^T of a published tile with a new sVref (positions from LDS).
+__device__ __forceinline__ void fp_restage_v(FBuf& b, const uint16_t* __restrict__ Vh, int L,
+                                             float inv_vref) {
+  uint32_t big = 0;
+#pragma unroll
+  for (int i = 0; i < kFpVItems; ++i) {
+    v4u vw[2];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int p = b.pos[fp_vkey(i, s)];
+      vw[s] = v4u{0u, 0u, 0u, 0u};
+      if ((unsigned)p < (unsigned)L)
+        vw[s] = reinterpret_cast<const v4u*>(Vh + (size_t)p * kHeadDim)[fp_vchunk(i)];
+    }
+    fp_store_vpair(b, vw[0], vw[1], fp_vkey(i, 0), fp_vchunk(i), inv_vref, big);
+  }
+}
+
+// Visibility of this lane's 32 keys of a full-precision tile to row tq, bit
+// kh * 16 + r for accumulator register r of half-tile kh.  Without the band
+// every listed key is seen from its position on (padding has a position
+// past every row), so only the positions are read.
+__device__ __forceinline__ uint32_t fp_vis_mask(const FBuf& b, int tq, int half, bool band) {
+  uint32_t m = 0;
+#pragma unroll
+  for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+    for (int rg = 0; rg < 4; ++rg) {
+      const int e = kh * 32 + rg * 8 + half * 4;
+      const v4i p4 = *reinterpret_cast<const v4i*>(&b.pos[e]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) m |= (uint32_t)(p4[j] <= tq) << (kh * 16 + rg * 4 + j);
+    }
+  if (band) {
+    uint32_t mh = 0;
+#pragma unroll
+    for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        const int e = kh * 32 + rg * 8 + half * 4;
+        const v4i h4 = *reinterpret_cast<const v4i*>(&b.hi[e]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) mh |= (uint32_t)(tq <= h4[j]) << (kh * 16 + rg * 4 + j);
       }
-    }
-    b.pos[tid] = p;
-    b.hi[tid] = hi;
+    m &= mh;
   }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < (kTile * 16) / kThreads; ++i) {
-    const int q = tid + i * kThreads;
-    const int e = q >> 4, col = q & 15;
-    const int p = b.pos[e];
-    uint4 kw = make_uint4(0, 0, 0, 0), vw = make_uint4(0, 0, 0, 0);
-    if ((unsigned)p < (unsigned)L) {
-      kw = reinterpret_cast<const uint4*>(Kh + (size_t)p * kHeadDim)[col];
-      vw = reinterpret_cast<const uint4*>(Vh + (size_t)p * kHeadDim)[col];
-    }
-    *reinterpret_cast<uint4*>(b.k + e * kKPitchBf + col * 16) = kw;
-    const int slot = vslot(e);
-    const uint32_t vv[4] = {vw.x, vw.y, vw.z, vw.w};
-#pragma unroll
-    for (int i2 = 0; i2 < 4; ++i2) {
-      const int d = col * 8 + 2 * i2;
-      *reinterpret_cast<uint16_t*>(b.v + d * kVPitch + slot * 2) = (uint16_t)(vv[i2] & 0xffff);
-      *reinterpret_cast<uint16_t*>(b.v + (d + 1) * kVPitch + slot * 2) = (uint16_t)(vv[i2] >> 16);
-    }
-  }
+  return m;
 }
 
 // Online-softmax state of one 32-query block of a wave (each lane owns one
@@ -757,7 +904,7 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
       vref = ldexpf(1.0f, e);
     }
   }
-  const float inv_vref = 1.0f / vref;
+  float inv_vref = 1.0f / vref;
 
   // ---------------- segment A: quantized keys ----------------
   if (nq_tiles > 0) {
@@ -838,66 +985,99 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
       for (int ks = 0; ks < 8; ++ks) qb[ks] = *reinterpret_cast<const v8bf*>(qrow + ks * 16 + half * 8);
     }
     const int nft = (fp_count + kTile - 1) / kTile;
-    FBuf& fb = sm.f;
+    FpList fl;
+    fl.vl = vl;
+    fl.kq = kq_pos + (size_t)bj * n_kvblk * kTile;
+    fl.dummy = reinterpret_cast<const int32_t*>(Kh);
+    fl.nvl = nvl;
+    fl.nq0 = nq0;
+    fl.nqb = nqb;
+    fl.base = fp_base;
+    fl.count = fp_count;
+    fl.band_w = shift;
+    // prologue: tile 0 published, tile 1 in registers.  Tile f is computed
+    // from sm.f[f % 2] while tile f+1 (loaded during tile f-1) is written to
+    // the other buffer and the rows of tile f+2 (and the position words of
+    // tile f+3) are loaded; one barrier per tile.  Tiles past the end are
+    // staged as padding into the free buffer (no branch).
+    if (threadIdx.x == 0) sm.f[0].ovf = sm.f[1].ovf = -1;
+    FpRegs fr;
+    fp_load_words(fr, fl, 0);
+    fp_load(fr, fl, Kh, Vh, 0, L);
+    __syncthreads();
+    fp_store(sm.f[0], fr, inv_vref, 0, L);
+    fp_load(fr, fl, Kh, Vh, 1, L);
+    __syncthreads();
+    const v2h one2 = {(_Float16)1.0f, (_Float16)1.0f};
     for (int ft = 0; ft < nft; ++ft) {
-      __syncthreads();
-      stage_fp(fb, Kh, Vh, vl, nvl, kq_pos + (size_t)bj * n_kvblk * kTile, nq0, nqb, fp_base,
-               ft * kTile, fp_count, L, shift);
-      __syncthreads();
-      v8bf ka[2][8];
+      FBuf& cur = sm.f[ft & 1];
+      const uint32_t vis = fp_vis_mask(cur, tq, half, shift > 0);
+      {
+        // V of this tile outside the f16 range at the current sVref: raise
+        // sVref to 2^(E - 134) (every |V| / sVref of the tile below 2^8),
+        // rescale the accumulator (exact), restage the tile's V
+        const int ov = cur.ovf;
+        if ((ov >> 8) == ft) {
+          const int ex = max(-100, (ov & 0xff) - 134);
+          const float nv = fmaxf(vref, __builtin_ldexpf(1.0f, ex));
+          const float c = vref / nv;
 #pragma unroll
-      for (int kh = 0; kh < 2; ++kh)
+          for (int dg = 0; dg < 4; ++dg)
 #pragma unroll
-        for (int ks = 0; ks < 8; ++ks)
-          ka[kh][ks] = *reinterpret_cast<const v8bf*>(fb.k + (kh * 32 + col) * kKPitchBf + ks * 32 +
-                                                      half * 16);
-      v8bf phi[4], plo[4];
+            for (int r = 0; r < 16; ++r) st.acc[dg][r] *= c;
+          vref = nv;
+          inv_vref = 1.0f / nv;
+          fp_restage_v(cur, Vh, L, inv_vref);
+          __syncthreads();
+        }
+      }
       v16f sf[2];
 #pragma unroll
       for (int kh = 0; kh < 2; ++kh) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) sf[kh][r] = 0.0f;
 #pragma unroll
-        for (int ks = 0; ks < 8; ++ks)
-          sf[kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[kh][ks], qb[ks], sf[kh], 0, 0, 0);
+        for (int ks = 0; ks < 8; ++ks) {
+          const v8bf ka = *reinterpret_cast<const v8bf*>(cur.k + (kh * 32 + col) * kKPitchBf +
+                                                         ks * 32 + half * 16);
+          sf[kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[ks], sf[kh], 0, 0, 0);
+        }
       }
+      fp_store(sm.f[(ft + 1) & 1], fr, inv_vref, ft + 1, L);
+      fp_load(fr, fl, Kh, Vh, ft + 2, L);
       float mt = -INFINITY;
 #pragma unroll
       for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int e = key_of(kh, r, half);
-          const bool vis = (fb.pos[e] <= tq) & (tq <= fb.hi[e]);
-          mt = fmaxf(mt, vis ? sf[kh][r] * alpha_log2e : -INFINITY);
-        }
+        for (int r = 0; r < 16; ++r)
+          mt = fmaxf(mt, (vis >> (kh * 16 + r)) & 1 ? sf[kh][r] * alpha_log2e : -INFINITY);
       lazy_max(st, xhalf_max(mt));
       apply_corr(st);
+      // f16 weights against f16 V / sVref; the row sum adds the same f16 weights
+      v8h p[4];
       float ps = 0.0f;
 #pragma unroll
-      for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int e = key_of(kh, r, half);
-          const bool vis = (fb.pos[e] <= tq) & (tq <= fb.hi[e]);
-          const float ex = __builtin_amdgcn_exp2f(sf[kh][r] * alpha_log2e - st.m);
-          const float pv = vis ? ex : 0.0f;
-          ps += pv;
-          const float pp = pv * inv_vref;
-          const __bf16 hi = (__bf16)pp;
-          const __bf16 lo = (__bf16)(pp - (float)hi);
-          phi[kh * 2 + (r >> 3)][r & 7] = hi;
-          plo[kh * 2 + (r >> 3)][r & 7] = lo;
-        }
+      for (int i = 0; i < 16; ++i) {
+        const int kh = i >> 3, r = (i & 7) * 2;
+        const float e0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sf[kh][r], alpha_log2e, -st.m));
+        const float e1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sf[kh][r + 1], alpha_log2e, -st.m));
+        v2h pk;
+        pk[0] = (_Float16)((vis >> (kh * 16 + r)) & 1 ? e0 : 0.0f);
+        pk[1] = (_Float16)((vis >> (kh * 16 + r + 1)) & 1 ? e1 : 0.0f);
+        ps = __builtin_amdgcn_fdot2(pk, one2, ps, false);
+        p[kh * 2 + (r >> 3)][r & 7] = pk[0];
+        p[kh * 2 + (r >> 3)][(r & 7) + 1] = pk[1];
+      }
       st.l += ps;
 #pragma unroll
-      for (int dg = 0; dg < 4; ++dg)
+      for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-          const v8bf va = *reinterpret_cast<const v8bf*>(fb.v + (dg * 32 + col) * kVPitch + ks * 32 +
-                                                         half * 16);
-          st.acc[dg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, phi[ks], st.acc[dg], 0, 0, 0);
-          st.acc[dg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, plo[ks], st.acc[dg], 0, 0, 0);
+        for (int dg = 0; dg < 4; ++dg) {
+          const v8h va = *reinterpret_cast<const v8h*>(cur.v + (dg * 32 + col) * kVPitch +
+                                                       ks * 32 + half * 16);
+          st.acc[dg] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, p[ks], st.acc[dg], 0, 0, 0);
         }
+      __syncthreads();
     }
   }
 

@@ -81,6 +81,30 @@ def test_v_outlier_block(bits):
     assert rel <= gc.TOL_MAX and mx <= gc.TOL_MAX and mean <= gc.TOL_MEAN
 
 
+@pytest.mark.parametrize("bits", [16, 8])
+def test_fp_v_beyond_f16(bits):
+    """Full-precision V values far above the f16 range of V / sVref (1e5,
+    then -3e6 on another channel, at window positions): the scan raises
+    sVref twice and restages those tiles; rows that see the outliers are
+    bounded relative to their magnitude, the other channels absolutely."""
+    L, W = 600, 96
+    d = _inputs("v_beyond_f16", 1, 4, 1, L, W)
+    x = gen.bf16_bits_to_f32(d["V"])
+    x[..., 520, 7] = 1.0e5
+    x[..., 580, 20] = -3.0e6
+    d["V"] = gen.f32_to_bf16_bits(x)
+    shape = gc.hyq.Shape(B=1, Hq=4, Hkv=1, L=L, window=W, budget_ppm=30000, bits_kv=bits)
+    g = gc.run_gpu(shape, d)
+    idx, qz = gc.check_select_quant(shape, d, g)
+    O = orc.attention(d["Q"], d["K"], d["V"], W, bits, idx, qz)
+    Og = g["out"].reshape(O.shape)
+    rel = gc.scaled_error(Og, O)
+    keep = ~np.isin(np.arange(O.shape[-1]), [7, 20])
+    mx, mean = gc.attention_error(Og[..., keep], O[..., keep])
+    print(f"  scaled max {rel:.3e}; other channels max-abs {mx:.3e} mean-abs {mean:.3e}", flush=True)
+    assert rel <= gc.TOL_MAX and mx <= gc.TOL_MAX and mean <= gc.TOL_MEAN
+
+
 def test_deterministic_and_bf16_output():
     d = _inputs("det", 1, 8, 2, 900, 64)
     shape = gc.hyq.Shape(B=1, Hq=8, Hkv=2, L=900, window=64, budget_ppm=20000, bits_kv=8)
