@@ -64,6 +64,7 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef float v2f __attribute__((ext_vector_type(2)));
 
 constexpr int kTile = 64;
 #ifndef HYQ_ATTN_WAVES
@@ -557,37 +558,32 @@ __device__ __forceinline__ void fp_load(FpRegs& r, const FpList& f, const uint16
   fp_load_words(r, f, ft + 1);
 }
 
-// f16 V / sVref of one bf16 value held in the high half of w (sVref a power
-// of two: exact for bf16 values of that range, down to the f16 subnormals);
-// `big` collects the largest |V| bits of values whose ratio leaves the f16
-// range.
-__device__ __forceinline__ _Float16 fp_v16(uint32_t w, float inv_vref, uint32_t& big) {
-  const float x = __uint_as_float(w) * inv_vref;
-  if (!(fabsf(x) <= 65504.0f)) big = max(big, w & 0x7fffffffu);
-  return (_Float16)x;
-}
-
 // V^T stores of one key pair (adjacent slots from the even key's) and one
-// 16-byte chunk: channel d gets the 32-bit word (f16 of key 2m, of key 2m+1).
-__device__ __forceinline__ void fp_store_vpair(FBuf& b, v4u v0, v4u v1, int key0, int chunk,
-                                               float inv_vref, uint32_t& big) {
+// 16-byte chunk: channel d gets the 32-bit word (f16 of key 2m, of key 2m+1)
+// of V / sVref (sVref a power of two: exact for bf16 values of that range,
+// down to the f16 subnormals).  Returns the largest |V| of the pair's chunk.
+__device__ __forceinline__ float fp_store_vpair(FBuf& b, v4u v0, v4u v1, int key0, int chunk,
+                                                float inv_vref) {
   const int slot = vslot(key0);
+  float mx = 0.0f;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int d = chunk * 8 + 2 * j;
-    v2h lo, hi;
-    lo[0] = fp_v16(v0[j] << 16, inv_vref, big);
-    lo[1] = fp_v16(v1[j] << 16, inv_vref, big);
-    hi[0] = fp_v16(v0[j] & 0xffff0000u, inv_vref, big);
-    hi[1] = fp_v16(v1[j] & 0xffff0000u, inv_vref, big);
-    *reinterpret_cast<v2h*>(b.v + d * kVPitch + slot * 2) = lo;
-    *reinterpret_cast<v2h*>(b.v + (d + 1) * kVPitch + slot * 2) = hi;
+    const float a0 = __uint_as_float(v0[j] << 16), a1 = __uint_as_float(v1[j] << 16);
+    const float b0 = __uint_as_float(v0[j] & 0xffff0000u), b1 = __uint_as_float(v1[j] & 0xffff0000u);
+    mx = fmaxf(mx, fmaxf(fabsf(a0), fabsf(a1)));
+    mx = fmaxf(mx, fmaxf(fabsf(b0), fabsf(b1)));
+    const v2f lo = {a0 * inv_vref, a1 * inv_vref}, hi = {b0 * inv_vref, b1 * inv_vref};
+    *reinterpret_cast<v2h*>(b.v + d * kVPitch + slot * 2) = __builtin_convertvector(lo, v2h);
+    *reinterpret_cast<v2h*>(b.v + (d + 1) * kVPitch + slot * 2) = __builtin_convertvector(hi, v2h);
   }
+  return mx;
 }
 
 // Write a loaded tile to LDS: K rows as bf16, V^T as f16 V / sVref,
 // positions and last rows.  A V ratio outside the f16 range records
-// (tile << 8) | (largest biased exponent) in ovf.
+// (tile << 8) | (largest biased exponent of |V|) in ovf (a NaN is not
+// recorded: it stays a NaN in f16).
 __device__ __forceinline__ void fp_store(FBuf& b, const FpRegs& r, float inv_vref, int tag, int L) {
 #pragma unroll
   for (int i = 0; i < kFpPairs; ++i) {
@@ -599,21 +595,20 @@ __device__ __forceinline__ void fp_store(FBuf& b, const FpRegs& r, float inv_vre
       b.hi[e] = r.hi[i];
     }
   }
-  uint32_t big = 0;
+  float mx = 0.0f;
 #pragma unroll
   for (int i = 0; i < kFpVItems; ++i) {
     const unsigned k0 = (unsigned)r.vpos[2 * i] < (unsigned)L ? 0xffffffffu : 0u;
     const unsigned k1 = (unsigned)r.vpos[2 * i + 1] < (unsigned)L ? 0xffffffffu : 0u;
-    fp_store_vpair(b, r.v[2 * i] & k0, r.v[2 * i + 1] & k1, fp_vkey(i, 0), fp_vchunk(i),
-                   inv_vref, big);
+    mx = fmaxf(mx, fp_store_vpair(b, r.v[2 * i] & k0, r.v[2 * i + 1] & k1, fp_vkey(i, 0),
+                                  fp_vchunk(i), inv_vref));
   }
-  if (big != 0) atomicMax(&b.ovf, (tag << 8) | (int)(big >> 23));
+  if (!(mx * inv_vref <= 65504.0f)) atomicMax(&b.ovf, (tag << 8) | (int)(__float_as_uint(mx) >> 23));
 }
 
 // Rewrite the V^T of a published tile with a new sVref (positions from LDS).
 __device__ __forceinline__ void fp_restage_v(FBuf& b, const uint16_t* __restrict__ Vh, int L,
                                              float inv_vref) {
-  uint32_t big = 0;
 #pragma unroll
   for (int i = 0; i < kFpVItems; ++i) {
     v4u vw[2];
@@ -624,7 +619,7 @@ __device__ __forceinline__ void fp_restage_v(FBuf& b, const uint16_t* __restrict
       if ((unsigned)p < (unsigned)L)
         vw[s] = reinterpret_cast<const v4u*>(Vh + (size_t)p * kHeadDim)[fp_vchunk(i)];
     }
-    fp_store_vpair(b, vw[0], vw[1], fp_vkey(i, 0), fp_vchunk(i), inv_vref, big);
+    fp_store_vpair(b, vw[0], vw[1], fp_vkey(i, 0), fp_vchunk(i), inv_vref);
   }
 }
 
@@ -730,6 +725,36 @@ __device__ __forceinline__ void softmax_general(NState& ns, const SV (&s)[2], v8
       p[kh * 2 + (r >> 3)][r & 7] = hp;
     }
   ns.l += ps * __builtin_amdgcn_rcpf(fm);
+}
+
+// Softmax of one full-precision tile (logits of hidden keys already -inf):
+// raise the reference max when the tile's exceeds it by more than kLazy,
+// weights 2^(s * alpha * log2(e) - m) as f16 into p (the B operands of P V),
+// and their f16 sum into the row sum.  alpha > 0, so the tile max of the
+// scaled logits is the scaled max of the raw ones.
+__device__ __forceinline__ void fp_softmax(NState& st, const v16f (&sf)[2], float alpha_log2e,
+                                           v8h (&p)[4]) {
+  float mx = -INFINITY;
+#pragma unroll
+  for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sf[kh][r]);
+  lazy_max(st, xhalf_max(mx) * alpha_log2e);
+  apply_corr(st);
+  const v2h one2 = {(_Float16)1.0f, (_Float16)1.0f};
+  float ps = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int kh = i >> 3, r = (i & 7) * 2;
+    v2f e;
+    e[0] = __builtin_amdgcn_exp2f(__builtin_fmaf(sf[kh][r], alpha_log2e, -st.m));
+    e[1] = __builtin_amdgcn_exp2f(__builtin_fmaf(sf[kh][r + 1], alpha_log2e, -st.m));
+    const v2h pk = __builtin_convertvector(e, v2h);
+    ps = __builtin_amdgcn_fdot2(pk, one2, ps, false);
+    p[kh * 2 + (r >> 3)][r & 7] = pk[0];
+    p[kh * 2 + (r >> 3)][(r & 7) + 1] = pk[1];
+  }
+  st.l += ps;
 }
 
 // One tile of the quantized segment:
@@ -1008,10 +1033,13 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
     fp_store(sm.f[0], fr, inv_vref, 0, L);
     fp_load(fr, fl, Kh, Vh, 1, L);
     __syncthreads();
-    const v2h one2 = {(_Float16)1.0f, (_Float16)1.0f};
     for (int ft = 0; ft < nft; ++ft) {
       FBuf& cur = sm.f[ft & 1];
-      const uint32_t vis = fp_vis_mask(cur, tq, half, shift > 0);
+      // without the band the list is ascending: a tile whose last position
+      // is at or before the wave's first row is seen whole by every row
+      const bool full = shift == 0 && cur.pos[kTile - 1] <= t0;
+      uint32_t vis = ~0u;
+      if (!full) vis = fp_vis_mask(cur, tq, half, shift > 0);
       {
         // V of this tile outside the f16 range at the current sVref: raise
         // sVref to 2^(E - 134) (every |V| / sVref of the tile below 2^8),
@@ -1045,30 +1073,16 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
       }
       fp_store(sm.f[(ft + 1) & 1], fr, inv_vref, ft + 1, L);
       fp_load(fr, fl, Kh, Vh, ft + 2, L);
-      float mt = -INFINITY;
+      if (!full) {
 #pragma unroll
-      for (int kh = 0; kh < 2; ++kh)
+        for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          mt = fmaxf(mt, (vis >> (kh * 16 + r)) & 1 ? sf[kh][r] * alpha_log2e : -INFINITY);
-      lazy_max(st, xhalf_max(mt));
-      apply_corr(st);
-      // f16 weights against f16 V / sVref; the row sum adds the same f16 weights
-      v8h p[4];
-      float ps = 0.0f;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int kh = i >> 3, r = (i & 7) * 2;
-        const float e0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sf[kh][r], alpha_log2e, -st.m));
-        const float e1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sf[kh][r + 1], alpha_log2e, -st.m));
-        v2h pk;
-        pk[0] = (_Float16)((vis >> (kh * 16 + r)) & 1 ? e0 : 0.0f);
-        pk[1] = (_Float16)((vis >> (kh * 16 + r + 1)) & 1 ? e1 : 0.0f);
-        ps = __builtin_amdgcn_fdot2(pk, one2, ps, false);
-        p[kh * 2 + (r >> 3)][r & 7] = pk[0];
-        p[kh * 2 + (r >> 3)][(r & 7) + 1] = pk[1];
+          for (int r = 0; r < 16; ++r)
+            sf[kh][r] = (vis >> (kh * 16 + r)) & 1 ? sf[kh][r] : -INFINITY;
       }
-      st.l += ps;
+      // f16 weights against f16 V / sVref
+      v8h p[4];
+      fp_softmax(st, sf, alpha_log2e, p);
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
