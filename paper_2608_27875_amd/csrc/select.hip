@@ -64,45 +64,47 @@ __device__ __forceinline__ TopkWs topk_ws(uint32_t* base, int bj, int P) {
   return w;
 }
 
-// One workgroup per (b, h).  The head's t tail rows are staged through LDS
-// kTailRows at a time (each of the 4 row groups of threads loads a quarter,
-// all loads in flight at once); then thread d adds the staged values of
-// channel d in ascending row order, continuing from +0 over all t rows, which
-// gives qpart[b][h][d].  The score kernel adds the g heads of a group in head
-// order.  The first head of each group also clears the key histogram and
-// the top-k candidate count of its (b, j), which the next kernels fill.
+// One workgroup per (b, h, group of 16 channels), so that the short kernel
+// spreads over the chip.  The head's t tail rows are staged through LDS
+// kTailRows at a time (thread r loads the 32 bytes of row r); then lane d of
+// the first wave adds the staged values of channel d in ascending row order,
+// continuing from +0 over all t rows, which gives qpart[b][h][d].  The score
+// kernel adds the g heads of a group in head order.  The first workgroup of
+// each group also clears the key histogram and the top-k candidate count of
+// its (b, j), which the next kernels fill.
 constexpr int kTailRows = 256;
-constexpr int kTailThreads = 4 * kHeadDim;
+constexpr int kTailThreads = kTailRows;
+constexpr int kTailCh = 16;   // channels per workgroup
 __global__ void __launch_bounds__(kTailThreads)
 tail_proxy_kernel(const uint16_t* __restrict__ Q, float* __restrict__ qpart,
                   uint32_t* __restrict__ hist, uint32_t* __restrict__ tws, int Hq, int Hkv, int L,
                   int t, int P) {
-  __shared__ uint16_t rows[kTailRows][kHeadDim];
+  __shared__ uint4 rows[kTailRows][kTailCh / 8];
   const int g = Hq / Hkv;
-  const int bh = blockIdx.x;
-  const int d = threadIdx.x % kHeadDim, qr = threadIdx.x / kHeadDim;
-  if (bh % g == 0) {
+  const int bh = blockIdx.x, c0 = blockIdx.y * kTailCh;
+  if (bh % g == 0 && blockIdx.y == 0) {
     uint32_t* hj = hist + (size_t)(bh / g) * kSelHistBins;
     for (int i = threadIdx.x; i < kSelHistBins; i += kTailThreads) hj[i] = 0u;
-    if (threadIdx.x == 0) tws[(size_t)(bh / g) * topk_ws_words(P)] = 0u;
+    if (threadIdx.x < 4) tws[(size_t)(bh / g) * topk_ws_words(P) + threadIdx.x] = 0u;
   }
-  const uint16_t* q = Q + ((size_t)bh * L + (L - t)) * kHeadDim + d;
-  constexpr int kPer = kTailRows / 4;
+  const uint16_t* q = Q + ((size_t)bh * L + (L - t)) * kHeadDim + c0;
+  const int d = threadIdx.x;   // channel c0 + d for the adding lanes
   float a = 0.0f;
   for (int r0 = 0; r0 < t; r0 += kTailRows) {
     const int n = min(kTailRows, t - r0);
-    uint16_t v[kPer];
-#pragma unroll
-    for (int u = 0; u < kPer; ++u)   // rows past the tail re-read its last row (never added)
-      v[u] = q[(size_t)min(r0 + qr * kPer + u, t - 1) * kHeadDim];
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) rows[qr * kPer + u][d] = v[u];
+    // rows past the tail re-read its last row (never added)
+    const uint4* src = reinterpret_cast<const uint4*>(
+        q + (size_t)min(r0 + (int)threadIdx.x, t - 1) * kHeadDim);
+    const uint4 v0 = src[0], v1 = src[1];
+    rows[threadIdx.x][0] = v0;
+    rows[threadIdx.x][1] = v1;
     __syncthreads();
-    if (qr == 0) {
+    if (d < kTailCh) {
+      const uint16_t* col = reinterpret_cast<const uint16_t*>(&rows[0][0]) + d;
       for (int i0 = 0; i0 < n; i0 += 32) {   // 32 LDS reads in flight, then the adds in order
         uint16_t x[32];
 #pragma unroll
-        for (int i = 0; i < 32; ++i) x[i] = rows[min(i0 + i, kTailRows - 1)][d];
+        for (int i = 0; i < 32; ++i) x[i] = col[(size_t)min(i0 + i, kTailRows - 1) * kTailCh];
 #pragma unroll
         for (int i = 0; i < 32; ++i)
           if (i0 + i < n) a = a + bf16_bits_to_f32(x[i]);
@@ -110,13 +112,14 @@ tail_proxy_kernel(const uint16_t* __restrict__ Q, float* __restrict__ qpart,
     }
     __syncthreads();
   }
-  if (qr == 0) qpart[(size_t)bh * kHeadDim + d] = a;
+  if (d < kTailCh) qpart[(size_t)bh * kHeadDim + c0 + d] = a;
 }
 
 // Workgroup-local key histogram (top kSelHistBits bits of the order key),
 // flushed into the KV head's histogram in global memory.
-constexpr int kHistThreads = 1024;
-constexpr int kScoreRows = kHistThreads;   // keys per workgroup (one per thread)
+constexpr int kHistThreads = 1024;         // hist_kernel: one key per thread
+constexpr int kScoreThreads = 512;         // score_kernel: 64 keys per wave
+constexpr int kScoreRows = kScoreThreads;  // keys per score workgroup
 
 __device__ __forceinline__ void hist_clear(uint32_t* lh) {
   for (int i = threadIdx.x; i < kSelHistBins; i += blockDim.x) lh[i] = 0u;
@@ -136,7 +139,8 @@ __device__ __forceinline__ float xor2(float x) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xF, 0xF, true));
 }
 
-// Scores of 1024 prefix keys per workgroup, 64 per wave.  A key row is read
+// Scores of 512 prefix keys per workgroup (two workgroups per CU, so that one
+// computes while the other loads), 64 per wave.  A key row is read
 // by 4 lanes: lane c (0..3) of the row's group loads the 16-byte chunks c,
 // c+4, c+8, c+12 (channels 8c.., 32+8c.., 64+8c.., 96+8c.., eight each), so
 // one load instruction covers 16 rows, 64 contiguous bytes each.  The pinned
@@ -145,7 +149,7 @@ __device__ __forceinline__ float xor2(float x) {
 // of a pair holds v[l], its partner v[l + h]; float addition is
 // commutative, so both lanes get the bits of v[l] + v[l + h]), and steps
 // 4, 2, 1 are in-lane again.
-__global__ void __launch_bounds__(kHistThreads)
+__global__ void __launch_bounds__(kScoreThreads, 2)
 score_kernel(const uint16_t* __restrict__ K, const float* __restrict__ qpart,
              float* __restrict__ S, uint32_t* __restrict__ hist, int g, int L, int P) {
   __shared__ uint32_t lh[kSelHistBins];
@@ -248,7 +252,7 @@ hist_kernel(const float* __restrict__ S, uint32_t* __restrict__ hist, int P) {
   const int bj = blockIdx.x;
   hist_clear(lh);
   __syncthreads();
-  const int p = blockIdx.y * kScoreRows + threadIdx.x;
+  const int p = blockIdx.y * kHistThreads + threadIdx.x;
   if (p < P) atomicAdd(&lh[order_key(S[(size_t)bj * P + p]) >> kHistShift], 1u);
   __syncthreads();
   hist_flush(lh, hist + (size_t)bj * kSelHistBins);
@@ -504,16 +508,17 @@ hipError_t launch_select(const hyq_shape& s, const hyq_sizes& z, const uint16_t*
   // over the XCDs round-robin, so with B*Hkv a multiple of 8 every chunk of a
   // head (and its final top-k workgroup) runs on one XCD and shares that
   // XCD's L2.
-  const dim3 hg(BH, (z.P + kScoreRows - 1) / kScoreRows);
   if (s.selector == HYQ_SEL_COLMASS) {
     hist_zero_kernel<<<BH, 256, 0, st>>>(hist, tws, z.P);
     const hipError_t e = launch_colmass_scores(s, z, Q, K, scores, cm_ws, st);
     if (e != hipSuccess) return e;
-    hist_kernel<<<hg, kHistThreads, 0, st>>>(scores, hist, z.P);
+    hist_kernel<<<dim3(BH, (z.P + kHistThreads - 1) / kHistThreads), kHistThreads, 0, st>>>(
+        scores, hist, z.P);
   } else {
-    tail_proxy_kernel<<<s.B * s.Hq, kTailThreads, 0, st>>>(Q, qsum, hist, tws, s.Hq, s.Hkv, s.L,
-                                                           t, z.P);
-    score_kernel<<<hg, kHistThreads, 0, st>>>(K, qsum, scores, hist, g, s.L, z.P);
+    tail_proxy_kernel<<<dim3(s.B * s.Hq, kHeadDim / kTailCh), kTailThreads, 0, st>>>(
+        Q, qsum, hist, tws, s.Hq, s.Hkv, s.L, t, z.P);
+    score_kernel<<<dim3(BH, (z.P + kScoreRows - 1) / kScoreRows), kScoreThreads, 0, st>>>(
+        K, qsum, scores, hist, g, s.L, z.P);
   }
   const dim3 cg(BH, (z.P + kTopkThreads - 1) / kTopkThreads);
   topk_classify_kernel<<<cg, kTopkThreads, 0, st>>>(scores, hist, tws, z.P, z.k);
