@@ -202,6 +202,15 @@ def test_dcache_bad_geometry_rejected(lib, kw, max_extra):
         hyq.hyq_dcache_init(s, s.L + max_extra)
 
 
+def test_dcache_rejects_fp6_query_format(lib):
+    """HYQ_FMT_FP4Q6 only sets the prefill's query codes; a decode cache with it is refused."""
+    s = _dshape(bits_kv=4, kv_format=hyq.FMT_FP4Q6)
+    with pytest.raises(hyq.HyqError) as e:
+        hyq.hyq_dcache_init(s, s.L)
+    assert e.value.code in (hyq.HYQ_EUNSUPPORTED, hyq.HYQ_EINVAL)
+    hyq.hyq_dcache_init(_dshape(bits_kv=4, kv_format=hyq.FMT_FP4), s.L)   # FP4 caches are fine
+
+
 def test_decode_calls_reject_bad_arguments_before_launch(lib):
     s = _dshape(L=1000, window=64, budget_ppm=20000, bits_kv=8)
     c, z = hyq.hyq_dcache_init(s, 1200)

@@ -151,8 +151,9 @@ def _check_big(cfg, d, n_heads, n_rows, seed):
 
 @pytest.mark.timeout(300)
 def test_gqa_8k():
-    cfg, d = _big(gen.GQA_8K, 32, 256)
-    _check_big(cfg, d, 32, 256, seed=2)
+    """The 8k GQA layer checked in full: every query row of all 32 heads."""
+    cfg, d = _big(gen.GQA_8K, 32, 8192)
+    _check_big(cfg, d, 32, cfg["L"], seed=2)
 
 
 @pytest.mark.timeout(300)
