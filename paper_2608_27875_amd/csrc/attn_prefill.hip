@@ -32,13 +32,13 @@
 // V^T tile in LDS stores each 16-key group in the matching order
 // [0-3, 8-11, 4-7, 12-15].
 //
-// Quantized tiles run through a three-buffer LDS ring fed from registers:
-// while tile c is computed, tile c+1 (loaded into registers during tile
-// c-1) is converted and written to LDS and tile c+2 is loaded, so global
-// latency is covered by a whole tile and each barrier waits only for LDS
-// writes.  The P V product of tile c-1 is issued interleaved with the
-// softmax of tile c (one MFMA per weight pair) so that the matrix cores and
-// the vector ALUs overlap within each wave.
+// Quantized tiles run through LDS rings fed from registers (K four
+// buffers, V two): while tile c is computed, K(c+2) and V(c) (loaded into
+// registers during tile c-1) are converted and written to LDS and K(c+3),
+// V(c+1) are loaded, so global latency is covered by a whole tile and each
+// barrier waits only for LDS writes.  The P V product of tile c-1 is issued
+// interleaved with the softmax of tile c (one MFMA per weight pair) so that
+// the matrix cores and the vector ALUs overlap within each wave.
 //
 // V scales: with sVref a power of two >= every sV of the head, the ratio
 // sV/sVref = fm * 2^e is split into its mantissa fm in [1/2, 1) and its
