@@ -182,3 +182,52 @@ def test_batch4_16k_sweep(batch4_data, ppm, bits):
     cfg = gen.workload(gen.BATCH4_16K, budget_ppm=ppm, bits=bits)
     print(f"batch-4 16k budget {ppm} bits {bits}", flush=True)
     _check_big(cfg, batch4_data, 2, 256, seed=5 + ppm + bits)
+
+
+@pytest.mark.parametrize("bits", [8, 16])
+def test_prefill_in_a_hip_graph(bits):
+    """Selection, quantization and attention captured in one HIP graph: each
+    replay, with eager work and synchronizations in between, writes the same
+    indices, codes and output as the eager calls, bit for bit (the library
+    allocates nothing and clears its workspace with its own kernels)."""
+    import torch
+    L, W = 1000, 64
+    d = _inputs("graph_prefill", 1, 8, 2, L, W)
+    shape = gc.hyq.Shape(B=1, Hq=8, Hkv=2, L=L, window=W, budget_ppm=20000, bits_kv=bits)
+    Q, K, V = (gc.to_dev(d[n]) for n in ("Q", "K", "V"))
+    bufs = gc.hyq.alloc_buffers(shape, Q.device, 0)
+
+    def step():
+        gc.hyq.hyq_select_vertical(shape, Q, K, bufs["idx"], None, bufs["ws"])
+        gc.hyq.hyq_quantize(shape, Q, K, V, bufs["idx"], bufs["q_codes"], bufs["q_scale"],
+                            bufs["k_codes"], bufs["k_scale"], bufs["v_codes"], bufs["v_scale"],
+                            bufs["kq_pos"])
+        gc.hyq.hyq_attn_prefill(shape, Q, K, V, bufs["idx"], bufs["q_codes"], bufs["q_scale"],
+                                bufs["k_codes"], bufs["k_scale"], bufs["v_codes"],
+                                bufs["v_scale"], bufs["kq_pos"], 1.0 / np.sqrt(shape.D),
+                                bufs["out"], 0)
+
+    names = ("idx", "q_codes", "k_codes", "v_codes", "kq_pos", "out")
+    step()
+    torch.cuda.synchronize()
+    ref = {n: bufs[n].clone() for n in names}
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()                                   # warm the side stream before capture
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        step()
+    for i in range(4):
+        for n in names:
+            bufs[n].zero_()
+        bufs["out"].fill_(float("nan"))
+        junk = torch.randn(1 << 20, device="cuda").sum()     # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for n in names:
+            assert torch.equal(bufs[n], ref[n]), f"replay {i}: {n}"
+        del junk
