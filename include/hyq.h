@@ -13,7 +13,8 @@
  *   hyq_attn_prefill     Algorithm 2, Stage 3 / eq. (prefill_hybrid) of
  *                        Section 4.2: one causal online softmax over the
  *                        quantized keys and the full-precision vertical-line
- *                        and window keys.
+ *                        and window keys;
+ *   hyq_prefill          the three in order, as one call.
  *
  * Conventions for every call:
  *  - Tensor pointers are DEVICE pointers owned by the caller.  Nothing is
@@ -203,9 +204,11 @@ HYQ_API int hyq_quantize(const hyq_shape* shape, const void* Q, const void* K, c
  * Precision: quantized logits are exact int32 dot products scaled in
  * float32 (int codes) or the float32 results of the E4M3 / E2M1 x E4M3
  * MFMA; full-precision logits are bf16 x bf16 products accumulated in
- * float32; softmax weights enter the P.V products as f16 (quantized keys,
- * against exact f16 codes) or as a high + low pair of bf16 (full-precision
- * keys, against bf16 V); all accumulation is float32.
+ * float32; softmax weights enter the P.V products as f16, against exact
+ * f16 codes (quantized keys) or against V / sVref in f16 (full-precision
+ * keys: exact for bf16 V within 2^16 of the reference sVref, a power of two
+ * the kernel raises when a tile's V exceeds that range); all accumulation is
+ * float32.
  */
 HYQ_API int hyq_attn_prefill(const hyq_shape* shape, const void* Q, const void* K, const void* V,
                      const int32_t* idx, const int8_t* q_codes, const float* q_scale,
@@ -213,6 +216,20 @@ HYQ_API int hyq_attn_prefill(const hyq_shape* shape, const void* Q, const void* 
                      const void* v_codes, const float* v_scale,
                      const int32_t* kq_pos, float softmax_scale,
                      void* out, int32_t out_dtype, void* stream);
+
+/* hyq_prefill - Algorithm 2 as one call: hyq_select_vertical (with no
+ * scores output), hyq_quantize and hyq_attn_prefill on `stream`, in that
+ * order.  Arguments, layouts, ownership and sizes are those of the three
+ * calls (ws / ws_bytes: the selection workspace); the arguments of all
+ * three are validated before the first launch, so an invalid argument
+ * returns HYQ_EINVAL with nothing launched.  Allocates nothing and keeps no
+ * state, so the call can be captured in a HIP graph.
+ */
+HYQ_API int hyq_prefill(const hyq_shape* shape, const void* Q, const void* K, const void* V,
+                        int32_t* idx, int8_t* q_codes, float* q_scale, void* k_codes,
+                        float* k_scale, void* v_codes, float* v_scale, int32_t* kq_pos,
+                        float softmax_scale, void* out, int32_t out_dtype, void* ws,
+                        size_t ws_bytes, void* stream);
 
 /* ======================================================================
  * Decode: Algorithm 4 (Freeze, App. A.4) and Algorithm 3 (HyQuant Decode,

@@ -27,7 +27,7 @@ WIN_FIXED, WIN_BAND = 0, 1    # hyq_shape.window_mode
 SEL_PROXY, SEL_COLMASS = 0, 1  # hyq_shape.selector
 DECODE_WS = 64                # HYQ_DECODE_WS: staging buffer capacity
 EXPORTED = ("hyq_sizes_for", "hyq_select_vertical", "hyq_quantize", "hyq_attn_prefill",
-            "hyq_strerror", "hyq_last_error", "hyq_dcache_init", "hyq_freeze",
+            "hyq_prefill", "hyq_strerror", "hyq_last_error", "hyq_dcache_init", "hyq_freeze",
             "hyq_decode_append", "hyq_decode_attn", "hyq_decode_attn_noalloc")
 
 
@@ -108,6 +108,8 @@ def lib():
         L.hyq_quantize.argtypes = [ctypes.POINTER(_Shape)] + [P] * 12
         L.hyq_attn_prefill.argtypes = [ctypes.POINTER(_Shape)] + [P] * 11 + \
             [ctypes.c_float, P, ctypes.c_int32, P]
+        L.hyq_prefill.argtypes = [ctypes.POINTER(_Shape)] + [P] * 11 + \
+            [ctypes.c_float, P, ctypes.c_int32, P, ctypes.c_size_t, P]
         L.hyq_strerror.restype = ctypes.c_char_p
         L.hyq_strerror.argtypes = [ctypes.c_int]
         L.hyq_last_error.restype = ctypes.c_char_p
@@ -121,7 +123,7 @@ def lib():
                                       ctypes.c_size_t, P]
         L.hyq_decode_attn_noalloc.argtypes = [DC, P, ctypes.c_float, P, ctypes.c_int32, P]
         for f in ("hyq_sizes_for", "hyq_select_vertical", "hyq_quantize", "hyq_attn_prefill",
-                  "hyq_dcache_init", "hyq_freeze", "hyq_decode_append", "hyq_decode_attn",
+                  "hyq_prefill", "hyq_dcache_init", "hyq_freeze", "hyq_decode_append", "hyq_decode_attn",
                   "hyq_decode_attn_noalloc"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
@@ -269,6 +271,40 @@ def hyq_attn_prefill(shape: Shape, Q, K, V, idx, q_codes, q_scale, k_codes, k_sc
                                   ctypes.c_int32(out_dtype), _stream(stream)))
 
 
+def hyq_prefill(shape: Shape, Q, K, V, idx, q_codes, q_scale, k_codes, k_scale, v_codes,
+                v_scale, kq_pos, softmax_scale, out, out_dtype=0, ws=None, stream=None):
+    """Algorithm 2 as one call: selection, quantization and attention
+    (see include/hyq.h); the library checks all three before launching."""
+    torch = _torch()
+    z = hyq_sizes_for(shape)
+    dev, bf = _io(shape, Q, K, V)
+    u8 = (torch.uint8, torch.int8)
+    f32 = (torch.float32,)
+    i32 = (torch.int32,)
+    quant = shape.bits_kv != 16
+    sel = z["k"] > 0
+    out_bytes = shape.B * shape.Hq * shape.L * shape.D * (4 if out_dtype == 0 else 2)
+    odt = (torch.float32,) if out_dtype == 0 else (torch.bfloat16,)
+    a = [
+        _ptr(Q, "Q", Q.numel() * 2, bf, dev), _ptr(K, "K", K.numel() * 2, bf, dev),
+        _ptr(V, "V", V.numel() * 2, bf, dev),
+        _ptr(idx, "idx", z["idx_bytes"], i32, dev, allow_none=not sel),
+        _ptr(q_codes, "q_codes", z["q_codes_bytes"], u8, dev, allow_none=not quant),
+        _ptr(q_scale, "q_scale", z["q_scale_bytes"], f32, dev, allow_none=not quant),
+        _ptr(k_codes, "k_codes", z["k_codes_bytes"], u8, dev, allow_none=not quant),
+        _ptr(k_scale, "k_scale", z["kv_scale_bytes"], f32, dev, allow_none=not quant),
+        _ptr(v_codes, "v_codes", z["v_codes_bytes"], u8, dev, allow_none=not quant),
+        _ptr(v_scale, "v_scale", z["kv_scale_bytes"], f32, dev, allow_none=not quant),
+        _ptr(kq_pos, "kq_pos", z["kq_pos_bytes"], i32, dev, allow_none=not quant),
+    ]
+    o = _ptr(out, "out", out_bytes, odt, dev)
+    w = _ptr(ws, "ws", z["select_ws_bytes"], (torch.uint8, torch.int8, torch.float32), dev,
+             allow_none=not sel)
+    wsb = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().hyq_prefill(ctypes.byref(shape.c()), *a, ctypes.c_float(softmax_scale), o,
+                             ctypes.c_int32(out_dtype), w, ctypes.c_size_t(wsb), _stream(stream)))
+
+
 # --------------------------------------------------------------------------
 # convenience: buffers and the chained path
 # --------------------------------------------------------------------------
@@ -300,15 +336,13 @@ def alloc_buffers(shape: Shape, device, out_dtype: int = 0) -> dict:
 
 def prefill(shape: Shape, Q, K, V, bufs: dict, out_dtype: int = 0, stream=None,
             softmax_scale: float | None = None):
-    """select -> quantize -> attention (Algorithm 2) into ``bufs['out']``."""
+    """select -> quantize -> attention (Algorithm 2, one hyq_prefill call)
+    into ``bufs['out']``."""
     scale = 1.0 / math.sqrt(shape.D) if softmax_scale is None else softmax_scale
     b = bufs
-    hyq_select_vertical(shape, Q, K, b["idx"], None, b["ws"], stream)
-    hyq_quantize(shape, Q, K, V, b["idx"], b["q_codes"], b["q_scale"], b["k_codes"],
-                 b["k_scale"], b["v_codes"], b["v_scale"], b["kq_pos"], stream)
-    hyq_attn_prefill(shape, Q, K, V, b["idx"], b["q_codes"], b["q_scale"], b["k_codes"],
-                     b["k_scale"], b["v_codes"], b["v_scale"], b["kq_pos"], scale, b["out"],
-                     out_dtype, stream)
+    hyq_prefill(shape, Q, K, V, b["idx"], b["q_codes"], b["q_scale"], b["k_codes"], b["k_scale"],
+                b["v_codes"], b["v_scale"], b["kq_pos"], scale, b["out"], out_dtype, b["ws"],
+                stream)
     return b["out"]
 
 

@@ -269,16 +269,61 @@ HYQ_API int hyq_sizes_for(const hyq_shape* shape, hyq_sizes* out) {
   return ok();
 }
 
-HYQ_API int hyq_select_vertical(const hyq_shape* shape, const void* Q, const void* K, int32_t* idx,
-                        float* scores, void* ws, size_t ws_bytes, void* stream) {
-  hyq_sizes z;
-  const int rc = check_shape(shape, &z);
-  if (rc) return rc;
+// Argument checks of the three prefill calls (after check_shape), shared by
+// the calls themselves and by hyq_prefill, which runs all three before it
+// launches anything.
+static int check_select_args(const hyq_sizes& z, const void* Q, const void* K, const int32_t* idx,
+                             const void* ws, size_t ws_bytes) {
   if (z.k == 0) return ok();
   if (!Q || !K || !idx) return fail(HYQ_EINVAL, "Q, K and idx must be non-NULL");
   if (!ws || ws_bytes < z.select_ws_bytes)
     return fail(HYQ_EINVAL, "workspace too small: %zu bytes given, %zu needed", ws_bytes,
                 z.select_ws_bytes);
+  return ok();
+}
+
+static int check_quantize_args(const hyq_shape* shape, const hyq_sizes& z, const void* Q,
+                               const void* K, const void* V, const int32_t* idx,
+                               const void* q_codes, const void* q_scale, const void* k_codes,
+                               const void* k_scale, const void* v_codes, const void* v_scale,
+                               const void* kq_pos) {
+  if (shape->bits_kv == 16) return ok();
+  if (!Q || !K || !V || !q_codes || !q_scale)
+    return fail(HYQ_EINVAL, "Q, K, V, q_codes and q_scale must be non-NULL");
+  if (z.k > 0 && !idx) return fail(HYQ_EINVAL, "idx must be non-NULL when k > 0");
+  if (z.n_kvblk > 0 && (!k_codes || !k_scale || !v_codes || !v_scale || !kq_pos))
+    return fail(HYQ_EINVAL,
+                "k_codes, k_scale, v_codes, v_scale and kq_pos must be non-NULL when nQ > 0");
+  return ok();
+}
+
+static int check_attn_args(const hyq_shape* shape, const hyq_sizes& z, const void* Q,
+                           const void* K, const void* V, const int32_t* idx, const void* q_codes,
+                           const void* q_scale, const void* k_codes, const void* k_scale,
+                           const void* v_codes, const void* v_scale, const void* kq_pos,
+                           float softmax_scale, const void* out, int32_t out_dtype) {
+  if (!Q || !K || !V || !out) return fail(HYQ_EINVAL, "Q, K, V and out must be non-NULL");
+  if (out_dtype != 0 && out_dtype != 1)
+    return fail(HYQ_EINVAL, "out_dtype must be 0 (float32) or 1 (bf16), got %d", out_dtype);
+  if (!(softmax_scale > 0.0f) || softmax_scale == INFINITY)
+    return fail(HYQ_EINVAL, "softmax_scale must be positive and finite");
+  if (shape->bits_kv != 16) {
+    if (z.k > 0 && !idx) return fail(HYQ_EINVAL, "idx must be non-NULL when k > 0");
+    if (!q_codes || !q_scale) return fail(HYQ_EINVAL, "q_codes and q_scale must be non-NULL");
+    if (z.n_kvblk > 0 && (!k_codes || !k_scale || !v_codes || !v_scale || !kq_pos))
+      return fail(HYQ_EINVAL,
+                  "k_codes, k_scale, v_codes, v_scale and kq_pos must be non-NULL when nQ > 0");
+  }
+  return ok();
+}
+
+HYQ_API int hyq_select_vertical(const hyq_shape* shape, const void* Q, const void* K, int32_t* idx,
+                        float* scores, void* ws, size_t ws_bytes, void* stream) {
+  hyq_sizes z;
+  int rc = check_shape(shape, &z);
+  if (rc) return rc;
+  if (z.k == 0) return ok();
+  if ((rc = check_select_args(z, Q, K, idx, ws, ws_bytes))) return rc;
   const SelectWs w = select_ws(*shape, z, ws, scores);
   return hip_status(hyq::launch_select(*shape, z, static_cast<const uint16_t*>(Q),
                                        static_cast<const uint16_t*>(K), idx, w.scores, w.qsum,
@@ -290,15 +335,12 @@ HYQ_API int hyq_quantize(const hyq_shape* shape, const void* Q, const void* K, c
                  const int32_t* idx, int8_t* q_codes, float* q_scale, void* k_codes,
                  float* k_scale, void* v_codes, float* v_scale, int32_t* kq_pos, void* stream) {
   hyq_sizes z;
-  const int rc = check_shape(shape, &z);
+  int rc = check_shape(shape, &z);
   if (rc) return rc;
   if (shape->bits_kv == 16) return ok();
-  if (!Q || !K || !V || !q_codes || !q_scale)
-    return fail(HYQ_EINVAL, "Q, K, V, q_codes and q_scale must be non-NULL");
-  if (z.k > 0 && !idx) return fail(HYQ_EINVAL, "idx must be non-NULL when k > 0");
-  if (z.n_kvblk > 0 && (!k_codes || !k_scale || !v_codes || !v_scale || !kq_pos))
-    return fail(HYQ_EINVAL,
-                "k_codes, k_scale, v_codes, v_scale and kq_pos must be non-NULL when nQ > 0");
+  if ((rc = check_quantize_args(shape, z, Q, K, V, idx, q_codes, q_scale, k_codes, k_scale,
+                                v_codes, v_scale, kq_pos)))
+    return rc;
   return hip_status(
       hyq::launch_quantize(*shape, z, static_cast<const uint16_t*>(Q),
                            static_cast<const uint16_t*>(K), static_cast<const uint16_t*>(V), idx,
@@ -314,20 +356,11 @@ HYQ_API int hyq_attn_prefill(const hyq_shape* shape, const void* Q, const void* 
                      const float* v_scale, const int32_t* kq_pos, float softmax_scale,
                      void* out, int32_t out_dtype, void* stream) {
   hyq_sizes z;
-  const int rc = check_shape(shape, &z);
+  int rc = check_shape(shape, &z);
   if (rc) return rc;
-  if (!Q || !K || !V || !out) return fail(HYQ_EINVAL, "Q, K, V and out must be non-NULL");
-  if (out_dtype != 0 && out_dtype != 1)
-    return fail(HYQ_EINVAL, "out_dtype must be 0 (float32) or 1 (bf16), got %d", out_dtype);
-  if (!(softmax_scale > 0.0f) || softmax_scale == INFINITY)
-    return fail(HYQ_EINVAL, "softmax_scale must be positive and finite");
-  if (shape->bits_kv != 16) {
-    if (z.k > 0 && !idx) return fail(HYQ_EINVAL, "idx must be non-NULL when k > 0");
-    if (!q_codes || !q_scale) return fail(HYQ_EINVAL, "q_codes and q_scale must be non-NULL");
-    if (z.n_kvblk > 0 && (!k_codes || !k_scale || !v_codes || !v_scale || !kq_pos))
-      return fail(HYQ_EINVAL,
-                  "k_codes, k_scale, v_codes, v_scale and kq_pos must be non-NULL when nQ > 0");
-  }
+  if ((rc = check_attn_args(shape, z, Q, K, V, idx, q_codes, q_scale, k_codes, k_scale, v_codes,
+                            v_scale, kq_pos, softmax_scale, out, out_dtype)))
+    return rc;
   return hip_status(
       hyq::launch_attn_prefill(
           *shape, z, static_cast<const uint16_t*>(Q), static_cast<const uint16_t*>(K),
@@ -335,6 +368,29 @@ HYQ_API int hyq_attn_prefill(const hyq_shape* shape, const void* Q, const void* 
           static_cast<const uint8_t*>(k_codes), k_scale, static_cast<const uint8_t*>(v_codes),
           v_scale, kq_pos, softmax_scale, out, out_dtype, static_cast<hipStream_t>(stream)),
       "hyq_attn_prefill launch");
+}
+
+HYQ_API int hyq_prefill(const hyq_shape* shape, const void* Q, const void* K, const void* V,
+                        int32_t* idx, int8_t* q_codes, float* q_scale, void* k_codes,
+                        float* k_scale, void* v_codes, float* v_scale, int32_t* kq_pos,
+                        float softmax_scale, void* out, int32_t out_dtype, void* ws,
+                        size_t ws_bytes, void* stream) {
+  hyq_sizes z;
+  int rc = check_shape(shape, &z);
+  if (rc) return rc;
+  if ((rc = check_select_args(z, Q, K, idx, ws, ws_bytes))) return rc;
+  if ((rc = check_quantize_args(shape, z, Q, K, V, idx, q_codes, q_scale, k_codes, k_scale,
+                                v_codes, v_scale, kq_pos)))
+    return rc;
+  if ((rc = check_attn_args(shape, z, Q, K, V, idx, q_codes, q_scale, k_codes, k_scale, v_codes,
+                            v_scale, kq_pos, softmax_scale, out, out_dtype)))
+    return rc;
+  if ((rc = hyq_select_vertical(shape, Q, K, idx, nullptr, ws, ws_bytes, stream))) return rc;
+  if ((rc = hyq_quantize(shape, Q, K, V, idx, q_codes, q_scale, k_codes, k_scale, v_codes,
+                         v_scale, kq_pos, stream)))
+    return rc;
+  return hyq_attn_prefill(shape, Q, K, V, idx, q_codes, q_scale, k_codes, k_scale, v_codes,
+                          v_scale, kq_pos, softmax_scale, out, out_dtype, stream);
 }
 
 HYQ_API int hyq_dcache_init(const hyq_shape* prefill, int64_t max_tokens, hyq_dcache* cache,

@@ -102,6 +102,32 @@ def test_null_pointers_and_args_rejected_before_launch(lib):
     assert lib.hyq_attn_prefill(bad, *args, ctypes.c_float(0.1), fake, 0, N) == hyq.HYQ_EUNSUPPORTED
 
 
+def test_prefill_validates_all_three_stages_before_launch(lib):
+    """hyq_prefill checks the arguments of selection, quantization and
+    attention before it launches anything (no device exists here): a bad
+    argument of any stage returns EINVAL."""
+    s = ctypes.byref(shape().c())
+    z = hyq.hyq_sizes_for(shape())
+    N = None
+    fake = ctypes.c_void_p(0x1000)   # never dereferenced: validation fails first
+    ok_ws = ctypes.c_size_t(z["select_ws_bytes"])
+    args = [fake] * 11
+    # selection: workspace one byte short
+    assert lib.hyq_prefill(s, *args, ctypes.c_float(0.088), fake, 0, fake,
+                           ctypes.c_size_t(z["select_ws_bytes"] - 1), N) == hyq.HYQ_EINVAL
+    assert "workspace" in hyq.hyq_last_error()
+    # quantization: no kq_pos
+    qa = [fake] * 10 + [N]
+    assert lib.hyq_prefill(s, *qa, ctypes.c_float(0.088), fake, 0, fake, ok_ws, N) == hyq.HYQ_EINVAL
+    # attention: bad output dtype, non-positive scale, missing output
+    assert lib.hyq_prefill(s, *args, ctypes.c_float(0.088), fake, 2, fake, ok_ws, N) == hyq.HYQ_EINVAL
+    assert lib.hyq_prefill(s, *args, ctypes.c_float(0.0), fake, 0, fake, ok_ws, N) == hyq.HYQ_EINVAL
+    assert lib.hyq_prefill(s, *args, ctypes.c_float(0.088), N, 0, fake, ok_ws, N) == hyq.HYQ_EINVAL
+    bad = ctypes.byref(shape(D=96).c())
+    assert lib.hyq_prefill(bad, *args, ctypes.c_float(0.1), fake, 0, fake, ok_ws, N) == \
+        hyq.HYQ_EUNSUPPORTED
+
+
 def test_select_with_zero_budget_is_noop(lib):
     # k = 0: nothing to do, no pointer is needed, nothing is enqueued
     s = ctypes.byref(shape(budget_ppm=0).c())

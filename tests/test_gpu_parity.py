@@ -231,3 +231,24 @@ def test_prefill_in_a_hip_graph(bits):
         for n in names:
             assert torch.equal(bufs[n], ref[n]), f"replay {i}: {n}"
         del junk
+
+
+@pytest.mark.parametrize("bits,fmt", [(8, 0), (4, 3), (16, 0)], ids=["int8", "fp4q6", "bits16"])
+def test_prefill_single_call_matches_three_calls(bits, fmt):
+    """hyq_prefill writes the same indices, codes, scales, positions and
+    output as hyq_select_vertical + hyq_quantize + hyq_attn_prefill."""
+    import torch
+    L, W = 900, 64
+    d = _inputs("single_call", 1, 8, 2, L, W)
+    shape = gc.hyq.Shape(B=1, Hq=8, Hkv=2, L=L, window=W, budget_ppm=20000, bits_kv=bits,
+                         kv_format=fmt)
+    g = gc.run_gpu(shape, d)
+    Q, K, V = (gc.to_dev(d[n]) for n in ("Q", "K", "V"))
+    bufs = gc.hyq.alloc_buffers(shape, Q.device, 0)
+    gc.hyq.prefill(shape, Q, K, V, bufs)
+    torch.cuda.synchronize()
+    for n in ("idx", "q_codes", "q_scale", "k_codes", "k_scale", "v_codes", "v_scale", "kq_pos"):
+        np.testing.assert_array_equal(bufs[n].cpu().numpy().view(np.uint8),
+                                      np.ascontiguousarray(g[n]).view(np.uint8), err_msg=n)
+    np.testing.assert_array_equal(bufs["out"].cpu().numpy().view(np.uint32),
+                                  g["out"].view(np.uint32))
