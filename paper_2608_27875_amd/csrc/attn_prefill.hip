@@ -805,6 +805,10 @@ __device__ __forceinline__ void segA_tile(Smem& sm, const SegA& a, int c, const 
   const float cqk = a.cq * sk;
   const float bias = __builtin_amdgcn_logf(fm) - st.m;   // log2
   const v2h one2 = {(_Float16)1.0f, (_Float16)1.0f};
+  // The wave in this loop issues ahead of its SIMD partner while that one
+  // stages and runs its S^T MFMAs (measured: 1-2% faster than equal
+  // priorities; raising the S^T part instead is slower).
+  __builtin_amdgcn_s_setprio(1);
   float ps = 0.0f;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
@@ -825,6 +829,7 @@ __device__ __forceinline__ void segA_tile(Smem& sm, const SegA& a, int c, const 
   // keep the fast-path weights computed here, next to the MFMAs, rather
   // than sunk into the branch below that consumes them
   asm volatile("" : "+v"(pcur[0]), "+v"(pcur[1]), "+v"(pcur[2]), "+v"(pcur[3]), "+v"(ps));
+  __builtin_amdgcn_s_setprio(0);
   const bool diag = last > a.t0;
   const bool redo = diag || __ballot(!(ps <= kFastMax)) != 0;
   if (redo) {
