@@ -551,6 +551,30 @@ def main():
                    "overlap_with_tail_proxy": round(float(np.mean(agree)), 4)}
         del bc
 
+    # how well each selector finds vertical lines that the attention itself
+    # makes (gen.shared_direction: a query direction shared by every query of
+    # a KV group, planted keys along it), at the same shape and budget
+    shared = None
+    if not args.no_colmass and z["k"]:
+        print("[bench] selector recall on shared-direction inputs", file=sys.stderr, flush=True)
+        ds = gen.shared_direction(0, B=shape.B, Hq=shape.Hq, Hkv=shape.Hkv, L=shape.L,
+                                  D=shape.D, W=shape.window, plant=cfg["plant"])
+        Qs, Ks = t(ds["Q"]), t(ds["K"])
+        shared = {"alpha": 7.0, "beta": 4.0}
+        for name, sel in (("tail_proxy", hyq.SEL_PROXY), ("column_mass", hyq.SEL_COLMASS)):
+            sx = dataclasses.replace(shape, selector=sel)
+            bx = hyq.alloc_buffers(sx, dev, out_dtype)
+            hyq.hyq_select_vertical(sx, Qs, Ks, bx["idx"], None, bx["ws"], stream)
+            got = bx["idx"].cpu().numpy().reshape(-1, z["k"])
+            rr = []
+            for bj in range(shape.B * shape.Hkv):
+                pp = [p for p in ds["planted"][bj].tolist() if p < z["P"]]
+                if pp:
+                    rr.append(len(set(pp) & set(got[bj].tolist())) / min(len(pp), z["k"]))
+            shared[name + "_recall"] = round(float(np.mean(rr)), 4) if rr else None
+            del bx
+        del Qs, Ks, ds
+
     flops = causal_flops(shape.B, shape.Hq, shape.L, shape.D)
     value = flops / (ms_step * 1e-3) / 1e12
     attn_tflops = flops / (attn_ms * 1e-3) / 1e12
@@ -609,6 +633,7 @@ def main():
         "four_bit_same_inputs": four_bit,
         "band_window_same_inputs": band,
         "colmass_selector_same_inputs": colmass,
+        "selector_recall_shared_direction": shared,
         "attention_tflops": round(attn_tflops, 2),
         "frac_int8_peak": round(attn_tflops / INT8_PEAK_TOPS, 4),
         "frac_blended_ceiling": round(attn_tflops / BLENDED_PEAK, 4),

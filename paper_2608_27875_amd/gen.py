@@ -97,6 +97,42 @@ def generate(seed: int, stream: int, B: int, Hq: int, Hkv: int, L: int, D: int,
     return dict(Q=Q, K=K, V=V, planted=planted)
 
 
+def shared_direction(seed: int, B: int, Hq: int, Hkv: int, L: int, D: int, W: int,
+                     plant: float, alpha: float = 7.0, beta: float = 4.0,
+                     outliers=OUTLIER_CHANNELS, **_unused):
+    """Inputs whose vertical lines come from the attention itself, to judge
+    how well a selector finds them: every query of KV group j carries beta *
+    e_j (a random unit direction per KV head) on top of N(0, 1), and the
+    planted keys (position 0 plus a fraction of random positions) carry
+    alpha * e_j, so each planted key gets a logit boost of about
+    alpha * beta / sqrt(D) from every query, not only from the tail.  V ~
+    N(0, 1); the outlier K channels are scaled by 10 as in ``generate``.
+    Returns the same fields as ``generate``."""
+    if Hq % Hkv:
+        raise ValueError("Hq must be a multiple of Hkv")
+    g = Hq // Hkv
+    rng = np.random.default_rng([int(seed), 1000 + int(L)])
+    Qf = rng.standard_normal((B, Hq, L, D), dtype=np.float32)
+    Kf = rng.standard_normal((B, Hkv, L, D), dtype=np.float32)
+    V = f32_to_bf16_bits(rng.standard_normal((B, Hkv, L, D), dtype=np.float32))
+    n_plant = min(L - 1, int(np.floor(plant * L + 0.5)))
+    planted = []
+    for b in range(B):
+        for j in range(Hkv):
+            e = rng.standard_normal(D)
+            e = (e / np.sqrt(np.dot(e, e))).astype(np.float32)
+            Qf[b, j * g:(j + 1) * g] += np.float32(beta) * e
+            pos = np.concatenate([[0], rng.choice(np.arange(1, L), n_plant, replace=False)]) \
+                if L > 1 else np.array([0])
+            pos = np.sort(pos.astype(np.int64))
+            Kf[b, j, pos, :] += np.float32(alpha) * e
+            planted.append(pos)
+    for c in outliers:
+        if c < D:
+            Kf[..., c] *= np.float32(10.0)
+    return dict(Q=f32_to_bf16_bits(Qf), K=f32_to_bf16_bits(Kf), V=V, planted=planted)
+
+
 def workload(name: str, **overrides) -> dict:
     """Parameters of a named workload (without its generator stream)."""
     cfg = {k: v for k, v in WORKLOADS[name].items() if k != "stream"}

@@ -150,3 +150,27 @@ def test_colmass_batch4_16k():
     mx, mean = gc.attention_error(Og, O)
     print(f"  max-abs {mx:.3e} mean-abs {mean:.3e}", flush=True)
     assert mx <= gc.TOL_MAX and mean <= gc.TOL_MEAN
+
+
+def test_shared_direction_both_selectors():
+    """Vertical lines made by the attention itself (gen.shared_direction): both
+    GPU selectors give the oracle's positions (Algorithm 1 bit for bit, its
+    scores too; the column mass within REL), and both find most planted
+    lines."""
+    B, Hq, Hkv, L, W, ppm = 1, 8, 2, 8192, 128, 20000
+    print("case shared_direction 8k", flush=True)
+    d = gen.shared_direction(0, B=B, Hq=Hq, Hkv=Hkv, L=L, D=128, W=W, plant=0.01)
+    base = hyq.Shape(B=B, Hq=Hq, Hkv=Hkv, L=L, window=W, budget_ppm=ppm, bits_kv=8)
+    g1 = gc.run_gpu(base, d)
+    idx1, _ = gc.check_select_quant(base, d, g1)
+    shape = dataclasses.replace(base, selector=COL)
+    g2 = gc.run_gpu(shape, d)
+    idx2 = check_colmass(shape, d, g2)
+    z = g1["sizes"]
+    for name, idx in (("tail proxy", idx1), ("column mass", idx2)):
+        rec = []
+        for bj, pos in enumerate(d["planted"]):
+            pp = set(p for p in pos.tolist() if p < z["P"])
+            rec.append(len(pp & set(idx.reshape(-1, z["k"])[bj].tolist())) / min(len(pp), z["k"]))
+        print(f"  {name} recall {np.mean(rec):.3f}", flush=True)
+        assert np.mean(rec) >= 0.7
