@@ -16,9 +16,9 @@
 //              window), 64 at a time gathered into two alternating LDS
 //              buffers a tile ahead through registers: S^T with the bf16
 //              MFMA; P V with the f16 MFMA on V / sVref converted to f16
-//              (exact for bf16 values of that range), or, for a tile whose
-//              V / sVref leaves the f16 range, with the bf16 MFMA on raw V
-//              and P split into a high and a low bf16 part (~16 bits).
+//              (exact for bf16 values of that range); a tile whose V / sVref
+//              leaves the f16 range raises sVref (the accumulator rescaled
+//              exactly) and is staged again.
 // Causality is by original key position in every segment.  With the
 // per-query window (HYQ_WIN_BAND) row t sees keys t+1-W .. t in full
 // precision and a quantized key only once it is older than that: segment A
