@@ -906,7 +906,9 @@ attn_prefill_kernel(const uint16_t* __restrict__ Q, const uint16_t* __restrict__
   } else {
     nvl = count_le(vl, k, t_last);
     const int tq_last = t_last - shift;        // last quantized position any row sees
-    const int nq_vis = tq_last < 0 ? 0 : (tq_last < P ? (tq_last + 1) - count_le(vl, k, tq_last) : nQ);
+    // (for the fixed window tq_last = t_last: the count is nvl, no second search)
+    const int nq_vis = tq_last < 0 ? 0 : (tq_last < P ? (tq_last + 1) -
+                                          (shift == 0 ? nvl : count_le(vl, k, tq_last)) : nQ);
     nq_tiles = min((nq_vis + kTile - 1) / kTile, n_kvblk);
     fp_base = P;
     if (band_w > 0) {
