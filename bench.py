@@ -423,10 +423,12 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
-    sel = [e[0].elapsed_time(e[1]) for e in evs]
-    qnt = [e[1].elapsed_time(e[2]) for e in evs]
-    att = [e[2].elapsed_time(e[3]) for e in evs]
-    attn_ms = float(np.mean(att))
+    # per-phase HIP-event times of the timed steps, reduced here once
+    phase_ms = {name: [e[a].elapsed_time(e[a + 1]) for e in evs]
+                for a, name in enumerate(("select", "quantize", "attention"))}
+    phase_mean = {k: float(np.mean(v)) for k, v in phase_ms.items()}
+    phase_median = {k: float(np.median(v)) for k, v in phase_ms.items()}
+    attn_ms = phase_mean["attention"]
 
     def median_ms(run, reps, pre=None, warm=1):
         """Median over `reps` launches of run(), timed with HIP events on the
@@ -467,7 +469,7 @@ def main():
         bits16 = {"attention_ms_median": round(ms16, 4),
                   "tflops": round(causal_flops(shape.B, shape.Hq, shape.L, shape.D) /
                                   (ms16 * 1e-3) / 1e12, 2),
-                  "speedup_of_hybrid": round(ms16 / float(np.median(att)), 3)}
+                  "speedup_of_hybrid": round(ms16 / phase_median["attention"], 3)}
         del b16
 
     def quant_attn_ms(sx, reps=10):
@@ -561,8 +563,8 @@ def main():
                                   D=shape.D, W=shape.window, plant=cfg["plant"])
         Qs, Ks = t(ds["Q"]), t(ds["K"])
         shared = {"alpha": 7.0, "beta": 4.0}
-        for name, sel in (("tail_proxy", hyq.SEL_PROXY), ("column_mass", hyq.SEL_COLMASS)):
-            sx = dataclasses.replace(shape, selector=sel)
+        for name, selector in (("tail_proxy", hyq.SEL_PROXY), ("column_mass", hyq.SEL_COLMASS)):
+            sx = dataclasses.replace(shape, selector=selector)
             bx = hyq.alloc_buffers(sx, dev, out_dtype)
             hyq.hyq_select_vertical(sx, Qs, Ks, bx["idx"], None, bx["ws"], stream)
             got = bx["idx"].cpu().numpy().reshape(-1, z["k"])
@@ -623,11 +625,11 @@ def main():
                      "unit": "TFLOP/s", "frac": round(attn_tflops / INT8_PEAK_TOPS, 4),
                      "traffic": traffic, "kernel": "attn_prefill_kernel"},
         "ms_per_layer": {"total": round(ms_step, 4), "attention": round(attn_ms, 4),
-                         "select": round(float(np.mean(sel)), 4),
-                         "quantize": round(float(np.mean(qnt)), 4)},
-        "ms_median": {"attention": round(float(np.median(att)), 4),
-                      "select": round(float(np.median(sel)), 4),
-                      "quantize": round(float(np.median(qnt)), 4)},
+                         "select": round(phase_mean["select"], 4),
+                         "quantize": round(phase_mean["quantize"], 4)},
+        "ms_median": {"attention": round(phase_median["attention"], 4),
+                      "select": round(phase_median["select"], 4),
+                      "quantize": round(phase_median["quantize"], 4)},
         "bits16_same_inputs": bits16,
         "fp8_same_inputs": fp8,
         "four_bit_same_inputs": four_bit,
@@ -637,8 +639,8 @@ def main():
         "attention_tflops": round(attn_tflops, 2),
         "frac_int8_peak": round(attn_tflops / INT8_PEAK_TOPS, 4),
         "frac_blended_ceiling": round(attn_tflops / BLENDED_PEAK, 4),
-        "select_gbs": round(sel_bytes / (np.mean(sel) * 1e-3) / 1e9, 1) if sel_bytes else None,
-        "quantize_gbs": round(q_bytes / (np.mean(qnt) * 1e-3) / 1e9, 1) if q_bytes else None,
+        "select_gbs": round(sel_bytes / (phase_mean["select"] * 1e-3) / 1e9, 1) if sel_bytes else None,
+        "quantize_gbs": round(q_bytes / (phase_mean["quantize"] * 1e-3) / 1e9, 1) if q_bytes else None,
         "planted_recall": round(float(np.mean(recall)), 4) if recall else None,
     }
     rec["decode"] = None if args.no_decode else decode_section(args.decode_layers,
